@@ -1,0 +1,339 @@
+"""CPU oracle for the UMAP layout path -- TEST INFRASTRUCTURE ONLY.
+
+Only the test suite, the package smoke check and the benchmark's CPU-baseline
+leg may import this package.  The product library never loads it, and it shares
+no code with the GPU path.  The arithmetic lives in ``umap_oracle.c`` (fp64
+state, fp32 schedule); this module marshals numpy arrays into it and adds two
+plain numpy routines (exact kNN and trustworthiness).
+
+Paper: Nolet et al., "Bringing UMAP Closer to the Speed of Light with GPU
+Acceleration" (AAAI 2021).  Each function cites the passage it follows.
+
+Parity status of each function is recorded next to it: "pinned" functions are
+checked by tests against closed forms, independent library routines or brute
+force; none is unpinned.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "umap_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+GCC_CMD = ["gcc", "-std=c11", "-O2", "-fopenmp", "-ffp-contract=off", "-fPIC", "-shared",
+           "-Wall", "-Wextra", "-o", _LIB, _SRC, "-lm"]
+
+
+def build() -> str:
+    """Compile the oracle library with gcc (always recompiles)."""
+    subprocess.run(GCC_CMD, check=True)
+    return _LIB
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build()
+        L = ctypes.CDLL(_LIB)
+        i32, i64, u32, u64, f64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32, ctypes.c_uint64, ctypes.c_double
+        P = ctypes.c_void_p
+        L.orc_philox4x32_10.argtypes = [P, P, P]
+        L.orc_philox_batch.argtypes = [P, i64, P, P]
+        L.orc_negative_vertex.argtypes = [u64, i64, i32, i32, i64]
+        L.orc_negative_vertex.restype = u32
+        L.orc_negative_batch.argtypes = [u64, i32, i64, i64, i32, i64, P]
+        L.orc_init.argtypes = [i64, i32, u64, P]
+        L.orc_smooth_knn.argtypes = [i64, i32, P, P, P]
+        L.orc_membership.argtypes = [i64, i32, P, P, P, P]
+        L.orc_fuzzy_union.argtypes = [i64, i32, P, P, P, P, P]
+        L.orc_fuzzy_union.restype = i64
+        L.orc_fit_ab.argtypes = [f64, f64, P, P]
+        L.orc_active.argtypes = [ctypes.c_float, i32]
+        L.orc_active.restype = ctypes.c_int
+        L.orc_prep.argtypes = [i64, P, P, P, i64, i32, P, P, P, P]
+        L.orc_prep.restype = i64
+        L.orc_attr_coef.argtypes = [f64, f64, f64]
+        L.orc_attr_coef.restype = f64
+        L.orc_rep_coef.argtypes = [f64, f64, f64]
+        L.orc_rep_coef.restype = f64
+        L.orc_epoch.argtypes = [i64, i32, P, P, P, f64, f64, i32, i32, u64, i32, P, P]
+        L.orc_epoch.restype = i64
+        L.orc_epoch_rows.argtypes = [i64, i32, P, P, P, f64, f64, i32, i32, u64, i32, P, i64, P, P]
+        L.orc_run.argtypes = [i64, i32, P, P, P, f64, f64, i32, i32, u64, P, P]
+        L.orc_num_threads.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _p(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _c(a, dtype):
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+def num_threads() -> int:
+    return int(lib().orc_num_threads())
+
+
+# --------------------------------------------------------------------------
+# Random streams (Philox4x32-10, SC'11).  Pinned against an independent
+# implementation of the same generator and by uniformity tests.
+# --------------------------------------------------------------------------
+
+def philox4x32_10(counters: np.ndarray, key: tuple[int, int]) -> np.ndarray:
+    ctr = _c(counters, np.uint32).reshape(-1, 4)
+    k = np.array(key, dtype=np.uint32)
+    out = np.empty_like(ctr)
+    lib().orc_philox_batch(_p(k), ctr.shape[0], _p(ctr), _p(out))
+    return out
+
+
+def negative_vertices(seed: int, epoch: int, e_first: int, count: int, neg_rate: int, n: int) -> np.ndarray:
+    out = np.empty((count, neg_rate), dtype=np.uint32)
+    lib().orc_negative_batch(seed, epoch, e_first, count, neg_rate, n, _p(out))
+    return out
+
+
+def init_layout(n: int, dim: int, seed: int) -> np.ndarray:
+    """Random initial layout, uniform on [-10, 10) (embedding-updates section)."""
+    out = np.empty((n, dim), dtype=np.float32)
+    lib().orc_init(n, dim, seed, _p(out))
+    return out
+
+
+# --------------------------------------------------------------------------
+# Neighbourhood weighting: Eq. 1 (smooth kNN) and Eq. 2 (fuzzy union).
+# --------------------------------------------------------------------------
+
+def smooth_knn(dists: np.ndarray) -> tuple[np.ndarray, np.ndarray]:
+    """rho and sigma per vertex (Eq. 1; neighbourhood-weighting section)."""
+    d = _c(dists, np.float32)
+    n, k = d.shape
+    rho = np.empty(n)
+    sigma = np.empty(n)
+    lib().orc_smooth_knn(n, k, _p(d), _p(rho), _p(sigma))
+    return rho, sigma
+
+
+def membership(dists: np.ndarray, rho: np.ndarray, sigma: np.ndarray) -> np.ndarray:
+    """A_ij = exp(-max(0, d_ij - rho_i) / sigma_i) (summand of Eq. 1)."""
+    d = _c(dists, np.float32)
+    n, k = d.shape
+    A = np.empty((n, k))
+    lib().orc_membership(n, k, _p(d), _p(_c(rho, np.float64)), _p(_c(sigma, np.float64)), _p(A))
+    return A
+
+
+def fuzzy_union(ids: np.ndarray, A: np.ndarray):
+    """B = A + A^T - A o A^T as COO sorted by (row, col), fp64 values (Eq. 2,
+    read with the t-conorm's minus sign)."""
+    ids = _c(ids, np.int32)
+    A = _c(A, np.float64)
+    n, k = ids.shape
+    cap = 2 * n * k
+    rows = np.empty(cap, dtype=np.int32)
+    cols = np.empty(cap, dtype=np.int32)
+    vals = np.empty(cap, dtype=np.float64)
+    m = lib().orc_fuzzy_union(n, k, _p(ids), _p(A), _p(rows), _p(cols), _p(vals))
+    if m < 0:
+        raise ValueError("invalid kNN lists (duplicate neighbour or id out of range)")
+    return rows[:m].copy(), cols[:m].copy(), vals[:m].copy()
+
+
+def fuzzy_graph(ids: np.ndarray, dists: np.ndarray):
+    """kNN lists -> symmetric COO graph with fp32 values (the layout's input)."""
+    rho, sigma = smooth_knn(dists)
+    A = membership(dists, rho, sigma)
+    r, c, v = fuzzy_union(ids, A)
+    return r, c, v.astype(np.float32)
+
+
+def fit_ab(spread: float = 1.0, min_dist: float = 0.1) -> tuple[float, float]:
+    """(a, b) of 1/(1 + a x^(2b)) fitted to the target curve of Eq. 3."""
+    a = ctypes.c_double()
+    b = ctypes.c_double()
+    lib().orc_fit_ab(spread, min_dist, ctypes.byref(a), ctypes.byref(b))
+    return a.value, b.value
+
+
+# --------------------------------------------------------------------------
+# Edge schedule and the ingest of B.
+# --------------------------------------------------------------------------
+
+def active(eps: float, epoch: int) -> bool:
+    return bool(lib().orc_active(np.float32(eps), epoch))
+
+
+def active_mask(eps: np.ndarray, epoch: int) -> np.ndarray:
+    """Vectorised predicate in fp32 (floor((n+1)/eps) > floor(n/eps))."""
+    e = _c(eps, np.float32)
+    now = np.floor(np.float32(epoch + 1) / e)
+    before = np.floor(np.float32(epoch) / e)
+    return now > before
+
+
+class Graph:
+    """Kept edges of B sorted by (head, tail) with a CSR index."""
+
+    def __init__(self, n, row_ptr, col, eps, w_max):
+        self.n = n
+        self.row_ptr = row_ptr
+        self.col = col
+        self.eps = eps
+        self.w_max = w_max
+
+    @property
+    def nnz(self) -> int:
+        return int(self.col.size)
+
+    def heads(self) -> np.ndarray:
+        return np.repeat(np.arange(self.n, dtype=np.int32), np.diff(self.row_ptr))
+
+
+class PrepError(ValueError):
+    def __init__(self, status: int):
+        super().__init__({-1: "invalid graph", -2: "asymmetric graph"}.get(status, str(status)))
+        self.status = status
+
+
+def prep(n: int, rows, cols, vals, n_epochs: int) -> Graph:
+    """Drop/prune/sort/eps of the COO graph (sparse-data handling section)."""
+    rows = _c(rows, np.int32)
+    cols = _c(cols, np.int32)
+    vals = _c(vals, np.float32)
+    nnz = rows.size
+    row_ptr = np.empty(n + 1, dtype=np.int64)
+    col = np.empty(max(nnz, 1), dtype=np.int32)
+    eps = np.empty(max(nnz, 1), dtype=np.float32)
+    w = ctypes.c_float()
+    kept = lib().orc_prep(n, _p(rows), _p(cols), _p(vals), nnz, n_epochs, _p(row_ptr), _p(col), _p(eps),
+                          ctypes.byref(w))
+    if kept < 0:
+        raise PrepError(int(kept))
+    return Graph(n, row_ptr, col[:kept].copy(), eps[:kept].copy(), w.value)
+
+
+# --------------------------------------------------------------------------
+# Layout SGD (objective of the UMAP section; embedding-updates and
+# reproducibility sections).
+# --------------------------------------------------------------------------
+
+def attr_coef(d2: float, a: float, b: float) -> float:
+    return lib().orc_attr_coef(d2, a, b)
+
+
+def rep_coef(d2: float, a: float, b: float) -> float:
+    return lib().orc_rep_coef(d2, a, b)
+
+
+def epoch(g: Graph, E: np.ndarray, epoch_idx: int, a: float, b: float, n_epochs: int, neg_rate: int,
+          seed: int) -> tuple[np.ndarray, int]:
+    """One Jacobi epoch from snapshot E (fp64 push form).  Returns (E', active)."""
+    E = _c(E, np.float64)
+    n, dim = E.shape
+    out = np.empty_like(E)
+    act = lib().orc_epoch(n, dim, _p(g.row_ptr), _p(g.col), _p(g.eps), a, b, n_epochs, neg_rate, seed,
+                          epoch_idx, _p(E), _p(out))
+    return out, int(act)
+
+
+def epoch_rows(g: Graph, E: np.ndarray, epoch_idx: int, a: float, b: float, n_epochs: int, neg_rate: int,
+               seed: int, which: np.ndarray) -> np.ndarray:
+    """Update landing on the vertices `which` in one epoch (push form)."""
+    E = _c(E, np.float64)
+    n, dim = E.shape
+    which = _c(which, np.int64)
+    delta = np.empty((which.size, dim))
+    lib().orc_epoch_rows(n, dim, _p(g.row_ptr), _p(g.col), _p(g.eps), a, b, n_epochs, neg_rate, seed,
+                         epoch_idx, _p(E), which.size, _p(which), _p(delta))
+    return delta
+
+
+def run(g: Graph, dim: int, a: float, b: float, n_epochs: int, neg_rate: int, seed: int):
+    """Init + all epochs.  Returns (E_N fp64, active counts per epoch)."""
+    E = np.empty((g.n, dim))
+    act = np.empty(n_epochs, dtype=np.int64)
+    rc = lib().orc_run(g.n, dim, _p(g.row_ptr), _p(g.col), _p(g.eps), a, b, n_epochs, neg_rate, seed,
+                       _p(E), _p(act))
+    if rc != 0:
+        raise MemoryError("oracle run failed")
+    return E, act
+
+
+# --------------------------------------------------------------------------
+# Plain numpy: exact kNN (kNN-graph section) and trustworthiness (Alg. 1;
+# Venna and Kaski's definition, which the experiments section cites).
+# --------------------------------------------------------------------------
+
+def _sqdist(A: np.ndarray, B: np.ndarray) -> np.ndarray:
+    A = A.astype(np.float64)
+    B = B.astype(np.float64)
+    d = (A * A).sum(1)[:, None] + (B * B).sum(1)[None, :] - 2.0 * (A @ B.T)
+    return np.maximum(d, 0.0)
+
+
+def exact_knn(X: np.ndarray, k: int, batch: int = 1024) -> tuple[np.ndarray, np.ndarray]:
+    """k nearest neighbours of every row (self excluded), Euclidean, ties by
+    smaller index.  Distances are recomputed exactly in fp64 for the chosen ids."""
+    X64 = X.astype(np.float64)
+    n = X.shape[0]
+    ids = np.empty((n, k), dtype=np.int32)
+    dist = np.empty((n, k), dtype=np.float32)
+    for s in range(0, n, batch):
+        t = min(n, s + batch)
+        D = _sqdist(X64[s:t], X64)
+        D[np.arange(t - s), np.arange(s, t)] = np.inf
+        cand = np.argpartition(D, k + 1, axis=1)[:, : k + 2]
+        cd = np.take_along_axis(D, cand, axis=1)
+        # exact fp64 distances of the candidates, then order by (distance, index)
+        diff = X64[s:t, None, :] - X64[cand]
+        ed = np.sqrt((diff * diff).sum(-1))
+        ed[~np.isfinite(cd)] = np.inf
+        order = np.lexsort((cand, ed), axis=1)[:, :k]
+        ids[s:t] = np.take_along_axis(cand, order, axis=1)
+        dist[s:t] = np.take_along_axis(ed, order, axis=1)
+    return ids, dist
+
+
+def trustworthiness(X: np.ndarray, Y: np.ndarray, k: int = 15, rows: np.ndarray | None = None,
+                    batch: int = 256) -> float:
+    """T(k) = 1 - 2/(n k (2n - 3k - 1)) * sum_i sum_{j in U_k(i)} (r(i, j) - k),
+    where U_k(i) are the embedding's k nearest neighbours of i that are not
+    among its k nearest input neighbours and r(i, j) is the 1-based rank of j
+    by input distance from i (self excluded, ties by index).  With `rows`, the
+    sum runs over those rows only and is rescaled by n / len(rows) (a sampled
+    estimate, identical for any two embeddings compared on the same rows)."""
+    n = X.shape[0]
+    if rows is None:
+        rows = np.arange(n)
+    rows = np.asarray(rows, dtype=np.int64)
+    X64 = X.astype(np.float64)
+    Y64 = Y.astype(np.float64)
+    total = 0.0
+    for s in range(0, rows.size, batch):
+        r = rows[s: s + batch]
+        DX = _sqdist(X64[r], X64)
+        DX[np.arange(r.size), r] = -np.inf          # self ranks first (rank 0)
+        DY = _sqdist(Y64[r], Y64)
+        DY[np.arange(r.size), r] = np.inf
+        nn_y = np.argpartition(DY, k, axis=1)[:, :k]
+        for t in range(r.size):
+            order = np.lexsort((np.arange(n), DX[t]))
+            rank = np.empty(n, dtype=np.int64)
+            rank[order] = np.arange(n)
+            rk = rank[nn_y[t]]
+            total += float(np.maximum(rk - k, 0).sum())
+    total *= n / rows.size
+    return 1.0 - 2.0 / (n * k * (2.0 * n - 3.0 * k - 1.0)) * total
