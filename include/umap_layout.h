@@ -1,0 +1,215 @@
+/*
+ * umap_layout.h -- C ABI of the MI355X (gfx950) layout-optimisation SGD of
+ * GPU UMAP (Nolet et al., "Bringing UMAP Closer to the Speed of Light with
+ * GPU Acceleration", AAAI 2021).
+ *
+ * What is computed.  Given the fuzzy union B (Eq. 2) of the neighbourhood
+ * graph as a symmetric weighted COO list, the library lays out n points in
+ * n_components dimensions by stochastic gradient descent on the cross-entropy
+ * objective of the UMAP section: every sampled edge (i, j) of B pulls both
+ * endpoints together (gradient of log Phi, Phi = 1/(1 + a d^(2b))), and each
+ * sampled edge draws neg_rate vertices uniformly at random that push the
+ * source away (gradient of log(1 - Phi)); embedding-updates section.  Edge e
+ * of weight w_e is sampled once every eps_e = w_max / w_e epochs.  Gradient
+ * components are clipped to [-4, 4]; the step size decays linearly,
+ * alpha_n = 1 - n / n_epochs.  Updates are epoch-synchronous: every read of
+ * epoch n sees the layout at the start of the epoch and all updates are applied
+ * at its end, which makes the result a deterministic function of the seed
+ * (the exactly-repeatable mode of the reproducibility section).
+ *
+ * Conventions.
+ *   - Every function returns UMAP_OK (0) or a negative UMAP_E_* code and, on
+ *     failure, sets a thread-local message readable with
+ *     umap_layout_last_error().  No C++ exception crosses the ABI.
+ *   - Out-parameters are left untouched on failure.
+ *   - Argument checks that need no GPU run before any HIP call.
+ *   - A handle belongs to the HIP device that was current at creation and is
+ *     used by one host thread at a time.  Work is enqueued on the handle's
+ *     stream (the null stream unless set); calls documented as blocking
+ *     synchronise that stream before returning.
+ *   - Layouts are row-major: element (i, d) of an n x n_components array is
+ *     at index i * n_components + d.  All embedding values are fp32.
+ */
+#ifndef UMAP_LAYOUT_H
+#define UMAP_LAYOUT_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define UMAP_OK 0
+#define UMAP_E_INVAL (-1)      /* an argument or the graph is invalid          */
+#define UMAP_E_ASYMMETRIC (-2) /* the kept graph is not symmetric              */
+#define UMAP_E_NOMEM (-3)      /* device or host allocation failed             */
+#define UMAP_E_DEVICE (-4)     /* no usable GPU, or a HIP call failed          */
+#define UMAP_E_STATE (-5)      /* call not valid in the handle's current state */
+
+typedef struct umap_layout umap_layout;
+
+typedef struct {
+    int64_t n;              /* vertices                                          */
+    int32_t n_components;   /* embedding dimension                               */
+    int32_t n_epochs;       /* N                                                 */
+    int32_t neg_rate;       /* negative samples per sampled edge                 */
+    int32_t epochs_done;    /* epochs run by the last run / run_epochs call      */
+    int64_t nnz_input;      /* entries passed to create                          */
+    int64_t nnz_kept;       /* edges kept after drop and prune                   */
+    int32_t max_degree;     /* largest kept row                                  */
+    float w_max;            /* largest kept weight                               */
+    int64_t active_edges;   /* sampled edges over the last call's epochs         */
+    int64_t edge_updates;   /* active_edges * (1 + neg_rate): positive samples
+                               plus drawn negatives (self draws included)        */
+    double prep_ms;         /* device time of the ingest inside create           */
+    double init_ms;         /* device time of the random initialisation (run)    */
+    double epochs_ms;       /* device time of the last call's epoch launches     */
+} umap_layout_stats_t;
+
+/*
+ * umap_layout_create -- ingest a host COO graph (sparse-data handling section:
+ * the COO list is sorted by row with a CSR index into it).
+ *
+ *   out           receives the handle (NULL on failure).
+ *   n             vertices, 1 <= n < 2^31.
+ *   n_components  embedding dimension, 1..16.
+ *   rows, cols    nnz int32 vertex ids in [0, n) (host memory, read only).
+ *   vals          nnz fp32 weights of B, finite (host memory, read only).
+ *   nnz           entries, 0 <= nnz < 2^31; nnz = 0 gives a graph without
+ *                 edges (a run only initialises the layout).
+ *   a, b          Phi(d) = 1 / (1 + a d^(2b)) (Eq. 3's smooth form), > 0.
+ *   n_epochs      1 <= N < 2^24.
+ *   neg_rate      negative samples per sampled edge, 0 <= R < 2^16.
+ *
+ * The inputs are copied; the caller keeps ownership.  On the device the
+ * ingest drops entries with val <= 0 and self loops, takes w_max = the largest
+ * remaining value, prunes entries with val < w_max / N (fp32), sorts the rest
+ * by (row, col) -- edge e is the position in that order -- and stores
+ * eps_e = w_max / val_e (fp32).  The kept graph must be symmetric: every
+ * kept (i, j, v) needs a kept (j, i) with bit-equal v.
+ * Errors: UMAP_E_INVAL (a scalar out of range, an index outside [0, n), a
+ * non-finite value, a kept (i, j) listed twice, a row too long for the
+ * accumulator), UMAP_E_ASYMMETRIC, UMAP_E_NOMEM, UMAP_E_DEVICE.  Blocking.
+ */
+int umap_layout_create(umap_layout **out, int64_t n, int32_t n_components, const int32_t *rows,
+                       const int32_t *cols, const float *vals, int64_t nnz, float a, float b,
+                       int32_t n_epochs, int32_t neg_rate);
+
+/*
+ * umap_layout_create_device -- as umap_layout_create, with rows, cols and
+ * vals in device memory of the current device (read only; the caller keeps
+ * ownership and may free them once the call returns).  `stream` (a
+ * hipStream_t, or NULL for the null stream) becomes the handle's stream.
+ * Index and value checks run on the device.  Blocking.
+ */
+int umap_layout_create_device(umap_layout **out, int64_t n, int32_t n_components, const int32_t *rows,
+                              const int32_t *cols, const float *vals, int64_t nnz, float a, float b,
+                              int32_t n_epochs, int32_t neg_rate, void *stream);
+
+/*
+ * umap_layout_run -- random initial layout, uniform on [-10, 10) per
+ * coordinate from the seed (embedding-updates section: random
+ * initialisation), then epochs 0 .. N-1.  Same seed, same graph: bit-identical
+ * output.  Blocking.
+ */
+int umap_layout_run(umap_layout *h, uint64_t seed);
+
+/*
+ * umap_layout_run_epochs -- epochs first .. last-1 (0 <= first <= last <= N)
+ * from the current layout, without initialisation.  Because the random
+ * streams are counter-based, running 0..m then m..N equals one run of 0..N.
+ * UMAP_E_STATE if no layout is present (no run and no set_embedding yet).
+ * Blocking.
+ */
+int umap_layout_run_epochs(umap_layout *h, uint64_t seed, int32_t first, int32_t last);
+
+/* umap_layout_get -- copy the n x n_components fp32 layout into host memory
+ * owned by the caller.  UMAP_E_STATE before the first run / set_embedding.
+ * Blocking. */
+int umap_layout_get(const umap_layout *h, float *out);
+
+/* umap_layout_get_device -- copy the layout into device memory `dev_out`
+ * (n x n_components fp32, caller-owned) on the handle's stream; not blocking.
+ * UMAP_E_STATE before the first run / set_embedding. */
+int umap_layout_get_device(const umap_layout *h, float *dev_out);
+
+/* umap_layout_set_embedding -- replace the layout with n x n_components fp32
+ * values from host memory (read only).  Blocking. */
+int umap_layout_set_embedding(umap_layout *h, const float *host);
+
+/* umap_layout_get_graph -- copy the kept graph to host memory: row_ptr
+ * (n + 1 int64), col (nnz_kept int32), eps (nnz_kept fp32).  Any array
+ * pointer may be NULL to skip it; nnz_kept may be NULL.  Blocking. */
+int umap_layout_get_graph(const umap_layout *h, int64_t *row_ptr, int32_t *col, float *eps,
+                          int64_t *nnz_kept);
+
+/* umap_layout_stats -- counters and device timings of the handle. */
+int umap_layout_stats(const umap_layout *h, umap_layout_stats_t *out);
+
+/* umap_layout_set_stream -- enqueue later work on `stream` (hipStream_t or
+ * NULL).  The caller keeps ownership of the stream and must keep it alive
+ * while the handle uses it. */
+int umap_layout_set_stream(umap_layout *h, void *stream);
+
+/* umap_layout_destroy -- free all device memory of the handle (waits for its
+ * stream).  NULL is a no-op. */
+void umap_layout_destroy(umap_layout *h);
+
+/* umap_layout_last_error -- message of the last failing call on this thread
+ * ("" if none).  Valid until the next failing call on this thread. */
+const char *umap_layout_last_error(void);
+
+/* ---- diagnostics (tests, measurement) ---------------------------------- */
+
+/* umap_layout_debug_active -- host array of nnz_kept bytes: 1 where edge e is
+ * sampled in `epoch` (floor((epoch + 1) / eps_e) > floor(epoch / eps_e),
+ * fp32), computed on the device.  Blocking. */
+int umap_layout_debug_active(const umap_layout *h, int32_t epoch, uint8_t *out);
+
+/* umap_layout_debug_negatives -- host array of count x neg_rate uint32: the
+ * negative-sample vertices the epoch kernel draws for edges
+ * e_first .. e_first + count - 1 in `epoch` with `seed`, computed on the device
+ * by the same routine.  0 <= e_first, e_first + count <= nnz_kept.  Blocking. */
+int umap_layout_debug_negatives(const umap_layout *h, uint64_t seed, int32_t epoch, int64_t e_first,
+                                int64_t count, uint32_t *out);
+
+/* umap_layout_set_kernel -- choose the epoch kernel: 0 = edge-parallel
+ * wavefront kernel (default), 1 = one thread per vertex.  Both compute the
+ * same result bit for bit. */
+int umap_layout_set_kernel(umap_layout *h, int32_t which);
+
+/* ---- input side --------------------------------------------------------- */
+
+/*
+ * umap_fuzzy_graph_device -- from a kNN graph (n x k neighbour ids and
+ * distances, row-major, device memory; neighbourhood-weighting section) build
+ * B on the device: rho_i (the smallest positive distance of row i), sigma_i
+ * (bisection so that sum_j exp(-max(0, d_ij - rho_i)/sigma_i) = log2 k, Eq. 1,
+ * floored at 1e-3 of the row's mean distance), A_ij, and the t-conorm
+ * A + A^T - A o A^T (Eq. 2), in fp64, rounded to fp32.
+ * Output: 2 n k COO slots in caller-owned device memory (rows, cols int32;
+ * vals fp32).  Slot i*k+s holds (i, j, B_ij) for j = ids[i*k+s]; slot
+ * n*k + i*k + s holds (j, i, B_ij) when i is not among j's neighbours and a
+ * placeholder of value 0 otherwise (placeholders and self entries are dropped
+ * by create).  Errors: UMAP_E_INVAL (n < 1, k < 1, k > 1024, 2nk >= 2^31, an
+ * id outside [0, n), a non-finite distance).  Blocking.
+ */
+int umap_fuzzy_graph_device(int64_t n, int32_t k, const int32_t *knn_ids, const float *knn_dists,
+                            int32_t *rows, int32_t *cols, float *vals, void *stream);
+
+/* umap_fit_ab -- least-squares (a, b) of 1/(1 + a x^(2b)) against Eq. 3's
+ * target (1 below min_dist, exp(-(x - min_dist)/spread) above) on 300 points
+ * of [0, 3 spread].  spread > 0, 0 <= min_dist < 3 spread.  Host only. */
+int umap_fit_ab(float spread, float min_dist, float *a, float *b);
+
+/* ---- roofline probes ---------------------------------------------------- */
+
+/* umap_probe_copy -- stream `bytes` (a multiple of 16) from src to dst on
+ * `stream` with 16-byte vector loads and stores; not blocking. */
+int umap_probe_copy(const void *src, void *dst, int64_t bytes, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* UMAP_LAYOUT_H */

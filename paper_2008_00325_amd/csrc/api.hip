@@ -1,0 +1,598 @@
+// api.hip -- host side of the C ABI declared in include/umap_layout.h.
+//
+// Argument checks that need no GPU run first; then one device arena holds
+// everything the handle keeps (CSR graph, wave partition, two embedding
+// buffers for the epoch-synchronous ping-pong, per-epoch counters), and a
+// stream-ordered scratch allocation holds the ingest's temporaries.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/umap_layout.h"
+#include "internal.hpp"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char *fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return code;
+}
+
+struct HipFailure {
+    hipError_t err;
+    const char *what;
+};
+
+#define UL_HIP(expr)                                    \
+    do {                                                \
+        hipError_t ul_e_ = (expr);                      \
+        if (ul_e_ != hipSuccess) throw HipFailure{ul_e_, #expr}; \
+    } while (0)
+
+int hip_fail(const HipFailure &f)
+{
+    if (f.err == hipErrorOutOfMemory || f.err == hipErrorMemoryAllocation)
+        return fail(UMAP_E_NOMEM, "device allocation failed (%s): %s", f.what, hipGetErrorString(f.err));
+    return fail(UMAP_E_DEVICE, "HIP call failed (%s): %s", f.what, hipGetErrorString(f.err));
+}
+
+// Optional failure injection for tests: UMAP_LAYOUT_FAULT=alloc makes the
+// arena allocation report out-of-memory; UMAP_LAYOUT_FAULT=launch@K makes the
+// launch of epoch K report a device error.  Nothing is launched in either case.
+bool fault_alloc()
+{
+    const char *f = getenv("UMAP_LAYOUT_FAULT");
+    return f && strcmp(f, "alloc") == 0;
+}
+
+int fault_launch_epoch()
+{
+    const char *f = getenv("UMAP_LAYOUT_FAULT");
+    if (!f || strncmp(f, "launch@", 7) != 0) return -1;
+    return atoi(f + 7);
+}
+
+size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
+
+struct Carver {
+    char *base;
+    size_t off = 0;
+    template <typename T>
+    T *take(size_t count)
+    {
+        T *p = reinterpret_cast<T *>(base + off);
+        off += align_up(count * sizeof(T) > 0 ? count * sizeof(T) : 1);
+        return p;
+    }
+};
+
+template <typename T>
+size_t need(size_t count)
+{
+    return align_up(count * sizeof(T) > 0 ? count * sizeof(T) : 1);
+}
+
+int check_scalars(int64_t n, int32_t dim, int64_t nnz, float a, float b, int32_t n_epochs, int32_t neg_rate)
+{
+    if (n < 1 || n >= ((int64_t)1 << 31)) return fail(UMAP_E_INVAL, "n must be in [1, 2^31), got %lld", (long long)n);
+    if (dim < 1 || dim > 16) return fail(UMAP_E_INVAL, "n_components must be in [1, 16], got %d", dim);
+    if (nnz < 0 || nnz >= ((int64_t)1 << 31)) return fail(UMAP_E_INVAL, "nnz must be in [0, 2^31), got %lld", (long long)nnz);
+    if (!(a > 0.0f) || !isfinite(a)) return fail(UMAP_E_INVAL, "a must be a positive finite value");
+    if (!(b > 0.0f) || !isfinite(b)) return fail(UMAP_E_INVAL, "b must be a positive finite value");
+    if (n_epochs < 1 || n_epochs >= (1 << 24)) return fail(UMAP_E_INVAL, "n_epochs must be in [1, 2^24), got %d", n_epochs);
+    if (neg_rate < 0 || neg_rate >= (1 << 16)) return fail(UMAP_E_INVAL, "neg_rate must be in [0, 2^16), got %d", neg_rate);
+    return UMAP_OK;
+}
+
+}  // namespace
+
+int ul::set_error(int code, const char *msg)
+{
+    g_err = msg;
+    return code;
+}
+
+struct umap_layout {
+    int device = 0;
+    hipStream_t stream = nullptr;
+    int64_t n = 0;
+    int32_t dim = 0;
+    float a = 0, b = 0;
+    int32_t n_epochs = 0, neg_rate = 0;
+    int64_t nnz_in = 0, nnz = 0;
+    int32_t max_degree = 0;
+    float w_max = 0;
+    int kernel = 0;
+
+    void *arena = nullptr;
+    int64_t *row_ptr = nullptr;
+    int32_t *col = nullptr;
+    float *eps = nullptr;
+    int32_t *part = nullptr;
+    int64_t n_waves = 0;
+    float *E[2] = {nullptr, nullptr};
+    int cur = 0;
+    bool has_layout = false;
+    unsigned long long *active = nullptr;   // n_epochs counters
+    hipEvent_t ev[3] = {nullptr, nullptr, nullptr};
+    umap_layout_stats_t st{};
+
+    void release()
+    {
+        if (stream || arena) hipStreamSynchronize(stream);
+        for (auto &e : ev)
+            if (e) hipEventDestroy(e);
+        if (arena) hipFree(arena);
+        arena = nullptr;
+    }
+};
+
+namespace {
+
+int create_common(umap_layout **out, int64_t n, int32_t dim, const int32_t *rows, const int32_t *cols,
+                  const float *vals, int64_t nnz, float a, float b, int32_t n_epochs, int32_t neg_rate,
+                  hipStream_t stream, bool host_inputs)
+{
+    umap_layout *h = new (std::nothrow) umap_layout();
+    if (!h) return fail(UMAP_E_NOMEM, "host allocation failed");
+    void *scratch = nullptr;
+    try {
+        int ndev = 0;
+        if (hipGetDeviceCount(&ndev) != hipSuccess || ndev < 1) {
+            delete h;
+            return fail(UMAP_E_DEVICE, "no HIP device available");
+        }
+        UL_HIP(hipGetDevice(&h->device));
+        h->stream = stream;
+        h->n = n;
+        h->dim = dim;
+        h->a = a;
+        h->b = b;
+        h->n_epochs = n_epochs;
+        h->neg_rate = neg_rate;
+        h->nnz_in = nnz;
+        for (auto &e : h->ev) UL_HIP(hipEventCreate(&e));
+
+        // persistent arena; the wave count is bounded with nnz (kept <= nnz)
+        const int wgt = ul::row_weight(dim);
+        const int64_t max_waves = (nnz + (int64_t)wgt * n) / ul::kWaveCost + 2;
+        const size_t nd = (size_t)n * (size_t)dim;
+        size_t bytes = need<int64_t>(n + 1) + need<int32_t>(nnz) + need<float>(nnz) + need<int32_t>(max_waves + 1) +
+                       2 * need<float>(nd) + need<unsigned long long>(n_epochs);
+        if (fault_alloc()) throw HipFailure{hipErrorOutOfMemory, "hipMalloc(arena) [injected]"};
+        UL_HIP(hipMalloc(&h->arena, bytes));
+        Carver cv{static_cast<char *>(h->arena)};
+        h->row_ptr = cv.take<int64_t>(n + 1);
+        h->col = cv.take<int32_t>(nnz);
+        h->eps = cv.take<float>(nnz);
+        h->part = cv.take<int32_t>(max_waves + 1);
+        h->E[0] = cv.take<float>(nd);
+        h->E[1] = cv.take<float>(nd);
+        h->active = cv.take<unsigned long long>(n_epochs);
+
+        // ingest scratch (stream-ordered)
+        ul::PrepBuffers B{};
+        B.nnz = nnz;
+        B.n = n;
+        B.n_epochs = n_epochs;
+        B.nblocks_scan = ul::scan_blocks(n);
+        size_t sbytes = 2 * need<int32_t>(n) + 2 * need<int32_t>(nnz) + 2 * need<float>(nnz) +
+                        need<int64_t>(B.nblocks_scan) + need<ul::PrepScalars>(1);
+        if (host_inputs) sbytes += 2 * need<int32_t>(nnz) + need<float>(nnz);
+        UL_HIP(hipMallocAsync(&scratch, sbytes, stream));
+        Carver sc{static_cast<char *>(scratch)};
+        B.deg = sc.take<int32_t>(n);
+        B.cursor = sc.take<int32_t>(n);
+        B.trow = sc.take<int32_t>(nnz);
+        B.tcol = sc.take<int32_t>(nnz);
+        B.tval = sc.take<float>(nnz);
+        B.sval = sc.take<float>(nnz);
+        B.bsum = sc.take<int64_t>(B.nblocks_scan);
+        B.scalars = sc.take<ul::PrepScalars>(1);
+        if (host_inputs) {
+            int32_t *dr = sc.take<int32_t>(nnz);
+            int32_t *dc = sc.take<int32_t>(nnz);
+            float *dv = sc.take<float>(nnz);
+            if (nnz) {
+                UL_HIP(hipMemcpyAsync(dr, rows, sizeof(int32_t) * nnz, hipMemcpyHostToDevice, stream));
+                UL_HIP(hipMemcpyAsync(dc, cols, sizeof(int32_t) * nnz, hipMemcpyHostToDevice, stream));
+                UL_HIP(hipMemcpyAsync(dv, vals, sizeof(float) * nnz, hipMemcpyHostToDevice, stream));
+            }
+            B.rows = dr;
+            B.cols = dc;
+            B.vals = dv;
+        } else {
+            B.rows = rows;
+            B.cols = cols;
+            B.vals = vals;
+        }
+        B.row_ptr = h->row_ptr;
+        B.col = h->col;
+        B.eps = h->eps;
+
+        UL_HIP(hipEventRecord(h->ev[0], stream));
+        UL_HIP(hipMemsetAsync(B.deg, 0, 2 * need<int32_t>(n), stream));   // deg and cursor are adjacent
+        UL_HIP(hipMemsetAsync(B.scalars, 0, sizeof(ul::PrepScalars), stream));
+        UL_HIP(ul::launch_prep(B, stream));
+        UL_HIP(hipEventRecord(h->ev[1], stream));
+
+        ul::PrepScalars S{};
+        int64_t kept = 0;
+        UL_HIP(hipMemcpyAsync(&S, B.scalars, sizeof S, hipMemcpyDeviceToHost, stream));
+        UL_HIP(hipMemcpyAsync(&kept, h->row_ptr + n, sizeof kept, hipMemcpyDeviceToHost, stream));
+        UL_HIP(hipStreamSynchronize(stream));
+        UL_HIP(hipFreeAsync(scratch, stream));
+        scratch = nullptr;
+
+        int rc = UMAP_OK;
+        if (S.flags & ul::kBadIndex) rc = fail(UMAP_E_INVAL, "a row or column index is outside [0, n)");
+        else if (S.flags & ul::kBadValue) rc = fail(UMAP_E_INVAL, "a value is not finite");
+        else if (S.flags & ul::kDuplicate) rc = fail(UMAP_E_INVAL, "an edge (i, j) is listed more than once");
+        else if (S.flags & ul::kAsymmetric)
+            rc = fail(UMAP_E_ASYMMETRIC, "the graph is not symmetric: a kept (i, j, v) has no (j, i) with equal v");
+        else if ((int64_t)S.max_degree * (8 + 4 * (int64_t)neg_rate) >= ((int64_t)1 << 31))
+            rc = fail(UMAP_E_INVAL, "a row of %d edges is too long for the fixed-point accumulator", S.max_degree);
+        if (rc != UMAP_OK) {
+            h->release();
+            delete h;
+            return rc;
+        }
+        h->nnz = kept;
+        h->max_degree = S.max_degree;
+        memcpy(&h->w_max, &S.wmax_bits, sizeof(float));
+        h->n_waves = (kept + (int64_t)wgt * n + ul::kWaveCost - 1) / ul::kWaveCost;
+        if (h->n_waves < 1) h->n_waves = 1;
+        UL_HIP(ul::launch_partition(h->row_ptr, n, dim, h->part, h->n_waves, stream));
+        float ms = 0;
+        UL_HIP(hipEventElapsedTime(&ms, h->ev[0], h->ev[1]));
+        h->st.prep_ms = ms;
+        *out = h;
+        return UMAP_OK;
+    } catch (const HipFailure &f) {
+        int rc = hip_fail(f);
+        if (scratch) hipFreeAsync(scratch, stream);
+        h->release();
+        delete h;
+        return rc;
+    } catch (...) {
+        if (scratch) hipFreeAsync(scratch, stream);
+        h->release();
+        delete h;
+        return fail(UMAP_E_NOMEM, "unexpected host failure");
+    }
+}
+
+int run_epochs_impl(umap_layout *h, uint64_t seed, int32_t first, int32_t last, bool timed_init)
+{
+    const int fault = fault_launch_epoch();
+    ul::EpochArgs A{};
+    A.n = (uint32_t)h->n;
+    A.neg_rate = h->neg_rate;
+    A.a = h->a;
+    A.b = h->b;
+    A.key_lo = (uint32_t)seed;
+    A.key_hi = (uint32_t)(seed >> 32);
+    UL_HIP(ul::launch_zero_u64(h->active, h->n_epochs, h->stream));
+    UL_HIP(hipEventRecord(h->ev[1], h->stream));
+    for (int32_t ep = first; ep < last; ++ep) {
+        if (ep == fault) {
+            UL_HIP(hipStreamSynchronize(h->stream));
+            return fail(UMAP_E_DEVICE, "epoch %d launch failed [injected]", ep);
+        }
+        A.E = h->E[h->cur];
+        A.E_next = h->E[1 - h->cur];
+        A.epoch = ep;
+        A.alpha = 1.0 - (double)ep / (double)h->n_epochs;
+        A.active_count = h->active + ep;
+        UL_HIP(ul::launch_epoch(h->kernel, h->dim, A, h->row_ptr, h->col, h->eps, h->part, h->n_waves, h->stream));
+        h->cur = 1 - h->cur;
+    }
+    UL_HIP(hipEventRecord(h->ev[2], h->stream));
+    std::vector<unsigned long long> act((size_t)h->n_epochs);
+    UL_HIP(hipMemcpyAsync(act.data(), h->active, sizeof(unsigned long long) * h->n_epochs, hipMemcpyDeviceToHost,
+                          h->stream));
+    UL_HIP(hipStreamSynchronize(h->stream));
+    unsigned long long total = 0;
+    for (int32_t ep = first; ep < last; ++ep) total += act[ep];
+    float ms = 0;
+    UL_HIP(hipEventElapsedTime(&ms, h->ev[1], h->ev[2]));
+    h->st.epochs_ms = ms;
+    if (timed_init) {
+        UL_HIP(hipEventElapsedTime(&ms, h->ev[0], h->ev[1]));
+        h->st.init_ms = ms;
+    }
+    h->st.epochs_done = last - first;
+    h->st.active_edges = (int64_t)total;
+    h->st.edge_updates = (int64_t)total * (1 + h->neg_rate);
+    return UMAP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *umap_layout_last_error(void) { return g_err.c_str(); }
+
+int umap_layout_create(umap_layout **out, int64_t n, int32_t n_components, const int32_t *rows, const int32_t *cols,
+                       const float *vals, int64_t nnz, float a, float b, int32_t n_epochs, int32_t neg_rate)
+{
+    try {
+        if (!out) return fail(UMAP_E_INVAL, "out is NULL");
+        *out = nullptr;
+        int rc = check_scalars(n, n_components, nnz, a, b, n_epochs, neg_rate);
+        if (rc) return rc;
+        if (nnz > 0 && (!rows || !cols || !vals)) return fail(UMAP_E_INVAL, "rows, cols and vals must not be NULL");
+        for (int64_t t = 0; t < nnz; ++t) {
+            if (rows[t] < 0 || rows[t] >= n || cols[t] < 0 || cols[t] >= n)
+                return fail(UMAP_E_INVAL, "entry %lld: index (%d, %d) outside [0, %lld)", (long long)t, rows[t],
+                            cols[t], (long long)n);
+            if (!isfinite(vals[t])) return fail(UMAP_E_INVAL, "entry %lld: value is not finite", (long long)t);
+        }
+        return create_common(out, n, n_components, rows, cols, vals, nnz, a, b, n_epochs, neg_rate, nullptr, true);
+    } catch (...) {
+        return fail(UMAP_E_NOMEM, "unexpected host failure");
+    }
+}
+
+int umap_layout_create_device(umap_layout **out, int64_t n, int32_t n_components, const int32_t *rows,
+                              const int32_t *cols, const float *vals, int64_t nnz, float a, float b, int32_t n_epochs,
+                              int32_t neg_rate, void *stream)
+{
+    try {
+        if (!out) return fail(UMAP_E_INVAL, "out is NULL");
+        *out = nullptr;
+        int rc = check_scalars(n, n_components, nnz, a, b, n_epochs, neg_rate);
+        if (rc) return rc;
+        if (nnz > 0 && (!rows || !cols || !vals)) return fail(UMAP_E_INVAL, "rows, cols and vals must not be NULL");
+        return create_common(out, n, n_components, rows, cols, vals, nnz, a, b, n_epochs, neg_rate,
+                             static_cast<hipStream_t>(stream), false);
+    } catch (...) {
+        return fail(UMAP_E_NOMEM, "unexpected host failure");
+    }
+}
+
+int umap_layout_run(umap_layout *h, uint64_t seed)
+{
+    if (!h) return fail(UMAP_E_INVAL, "handle is NULL");
+    try {
+        UL_HIP(hipSetDevice(h->device));
+        UL_HIP(hipEventRecord(h->ev[0], h->stream));
+        UL_HIP(ul::launch_init(h->E[h->cur], h->n, h->dim, seed, h->stream));
+        h->has_layout = true;
+        return run_epochs_impl(h, seed, 0, h->n_epochs, true);
+    } catch (const HipFailure &f) {
+        return hip_fail(f);
+    } catch (...) {
+        return fail(UMAP_E_NOMEM, "unexpected host failure");
+    }
+}
+
+int umap_layout_run_epochs(umap_layout *h, uint64_t seed, int32_t first, int32_t last)
+{
+    if (!h) return fail(UMAP_E_INVAL, "handle is NULL");
+    if (first < 0 || first > last || last > h->n_epochs)
+        return fail(UMAP_E_INVAL, "need 0 <= first <= last <= n_epochs (%d), got %d, %d", h->n_epochs, first, last);
+    if (!h->has_layout) return fail(UMAP_E_STATE, "no layout yet: call umap_layout_run or umap_layout_set_embedding");
+    try {
+        UL_HIP(hipSetDevice(h->device));
+        return run_epochs_impl(h, seed, first, last, false);
+    } catch (const HipFailure &f) {
+        return hip_fail(f);
+    } catch (...) {
+        return fail(UMAP_E_NOMEM, "unexpected host failure");
+    }
+}
+
+int umap_layout_get(const umap_layout *h, float *out)
+{
+    if (!h || !out) return fail(UMAP_E_INVAL, "handle or out is NULL");
+    if (!h->has_layout) return fail(UMAP_E_STATE, "no layout yet");
+    try {
+        UL_HIP(hipSetDevice(h->device));
+        UL_HIP(hipMemcpyAsync(out, h->E[h->cur], sizeof(float) * h->n * h->dim, hipMemcpyDeviceToHost, h->stream));
+        UL_HIP(hipStreamSynchronize(h->stream));
+        return UMAP_OK;
+    } catch (const HipFailure &f) {
+        return hip_fail(f);
+    }
+}
+
+int umap_layout_get_device(const umap_layout *h, float *dev_out)
+{
+    if (!h || !dev_out) return fail(UMAP_E_INVAL, "handle or dev_out is NULL");
+    if (!h->has_layout) return fail(UMAP_E_STATE, "no layout yet");
+    try {
+        UL_HIP(hipSetDevice(h->device));
+        UL_HIP(hipMemcpyAsync(dev_out, h->E[h->cur], sizeof(float) * h->n * h->dim, hipMemcpyDeviceToDevice,
+                              h->stream));
+        return UMAP_OK;
+    } catch (const HipFailure &f) {
+        return hip_fail(f);
+    }
+}
+
+int umap_layout_set_embedding(umap_layout *h, const float *host)
+{
+    if (!h || !host) return fail(UMAP_E_INVAL, "handle or host is NULL");
+    try {
+        UL_HIP(hipSetDevice(h->device));
+        UL_HIP(hipMemcpyAsync(h->E[h->cur], host, sizeof(float) * h->n * h->dim, hipMemcpyHostToDevice, h->stream));
+        UL_HIP(hipStreamSynchronize(h->stream));
+        h->has_layout = true;
+        return UMAP_OK;
+    } catch (const HipFailure &f) {
+        return hip_fail(f);
+    }
+}
+
+int umap_layout_get_graph(const umap_layout *h, int64_t *row_ptr, int32_t *col, float *eps, int64_t *nnz_kept)
+{
+    if (!h) return fail(UMAP_E_INVAL, "handle is NULL");
+    try {
+        UL_HIP(hipSetDevice(h->device));
+        if (row_ptr)
+            UL_HIP(hipMemcpyAsync(row_ptr, h->row_ptr, sizeof(int64_t) * (h->n + 1), hipMemcpyDeviceToHost, h->stream));
+        if (col && h->nnz)
+            UL_HIP(hipMemcpyAsync(col, h->col, sizeof(int32_t) * h->nnz, hipMemcpyDeviceToHost, h->stream));
+        if (eps && h->nnz)
+            UL_HIP(hipMemcpyAsync(eps, h->eps, sizeof(float) * h->nnz, hipMemcpyDeviceToHost, h->stream));
+        UL_HIP(hipStreamSynchronize(h->stream));
+        if (nnz_kept) *nnz_kept = h->nnz;
+        return UMAP_OK;
+    } catch (const HipFailure &f) {
+        return hip_fail(f);
+    }
+}
+
+int umap_layout_stats(const umap_layout *h, umap_layout_stats_t *out)
+{
+    if (!h || !out) return fail(UMAP_E_INVAL, "handle or out is NULL");
+    umap_layout_stats_t s = h->st;
+    s.n = h->n;
+    s.n_components = h->dim;
+    s.n_epochs = h->n_epochs;
+    s.neg_rate = h->neg_rate;
+    s.nnz_input = h->nnz_in;
+    s.nnz_kept = h->nnz;
+    s.max_degree = h->max_degree;
+    s.w_max = h->w_max;
+    *out = s;
+    return UMAP_OK;
+}
+
+int umap_layout_set_stream(umap_layout *h, void *stream)
+{
+    if (!h) return fail(UMAP_E_INVAL, "handle is NULL");
+    try {
+        UL_HIP(hipStreamSynchronize(h->stream));
+    } catch (const HipFailure &f) {
+        return hip_fail(f);
+    }
+    h->stream = static_cast<hipStream_t>(stream);
+    return UMAP_OK;
+}
+
+int umap_layout_set_kernel(umap_layout *h, int32_t which)
+{
+    if (!h) return fail(UMAP_E_INVAL, "handle is NULL");
+    if (which != 0 && which != 1) return fail(UMAP_E_INVAL, "kernel must be 0 or 1, got %d", which);
+    h->kernel = which;
+    return UMAP_OK;
+}
+
+void umap_layout_destroy(umap_layout *h)
+{
+    if (!h) return;
+    hipSetDevice(h->device);
+    h->release();
+    delete h;
+}
+
+int umap_layout_debug_active(const umap_layout *h, int32_t epoch, uint8_t *out)
+{
+    if (!h || !out) return fail(UMAP_E_INVAL, "handle or out is NULL");
+    if (epoch < 0 || epoch >= h->n_epochs) return fail(UMAP_E_INVAL, "epoch %d outside [0, %d)", epoch, h->n_epochs);
+    if (h->nnz == 0) return UMAP_OK;
+    uint8_t *d = nullptr;
+    try {
+        UL_HIP(hipSetDevice(h->device));
+        UL_HIP(hipMallocAsync((void **)&d, h->nnz, h->stream));
+        UL_HIP(ul::launch_debug_active(h->eps, h->nnz, epoch, d, h->stream));
+        UL_HIP(hipMemcpyAsync(out, d, h->nnz, hipMemcpyDeviceToHost, h->stream));
+        UL_HIP(hipFreeAsync(d, h->stream));
+        d = nullptr;
+        UL_HIP(hipStreamSynchronize(h->stream));
+        return UMAP_OK;
+    } catch (const HipFailure &f) {
+        if (d) hipFreeAsync(d, h->stream);
+        return hip_fail(f);
+    }
+}
+
+int umap_layout_debug_negatives(const umap_layout *h, uint64_t seed, int32_t epoch, int64_t e_first, int64_t count,
+                                uint32_t *out)
+{
+    if (!h || !out) return fail(UMAP_E_INVAL, "handle or out is NULL");
+    if (e_first < 0 || count < 0 || e_first + count > h->nnz)
+        return fail(UMAP_E_INVAL, "edge range [%lld, %lld) outside the %lld kept edges", (long long)e_first,
+                    (long long)(e_first + count), (long long)h->nnz);
+    if (count == 0 || h->neg_rate == 0) return UMAP_OK;
+    uint32_t *d = nullptr;
+    const size_t bytes = sizeof(uint32_t) * (size_t)count * (size_t)h->neg_rate;
+    try {
+        UL_HIP(hipSetDevice(h->device));
+        UL_HIP(hipMallocAsync((void **)&d, bytes, h->stream));
+        UL_HIP(ul::launch_debug_negatives((uint32_t)h->n, seed, epoch, e_first, count, h->neg_rate, d, h->stream));
+        UL_HIP(hipMemcpyAsync(out, d, bytes, hipMemcpyDeviceToHost, h->stream));
+        UL_HIP(hipFreeAsync(d, h->stream));
+        d = nullptr;
+        UL_HIP(hipStreamSynchronize(h->stream));
+        return UMAP_OK;
+    } catch (const HipFailure &f) {
+        if (d) hipFreeAsync(d, h->stream);
+        return hip_fail(f);
+    }
+}
+
+int umap_fuzzy_graph_device(int64_t n, int32_t k, const int32_t *knn_ids, const float *knn_dists, int32_t *rows,
+                            int32_t *cols, float *vals, void *stream)
+{
+    if (n < 1 || n >= ((int64_t)1 << 31)) return fail(UMAP_E_INVAL, "n must be in [1, 2^31)");
+    if (k < 1 || k > 1024) return fail(UMAP_E_INVAL, "k must be in [1, 1024], got %d", k);
+    if (2 * n * (int64_t)k >= ((int64_t)1 << 31)) return fail(UMAP_E_INVAL, "2 n k must be below 2^31");
+    if (!knn_ids || !knn_dists || !rows || !cols || !vals) return fail(UMAP_E_INVAL, "a pointer argument is NULL");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    void *scratch = nullptr;
+    try {
+        int ndev = 0;
+        if (hipGetDeviceCount(&ndev) != hipSuccess || ndev < 1) return fail(UMAP_E_DEVICE, "no HIP device available");
+        const int64_t np = ul::graph_partials(n, k);
+        size_t bytes = 2 * need<double>(n) + need<double>(np + 1) + need<unsigned>(1);
+        UL_HIP(hipMallocAsync(&scratch, bytes, s));
+        Carver cv{static_cast<char *>(scratch)};
+        double *rho = cv.take<double>(n);
+        double *sigma = cv.take<double>(n);
+        double *partial = cv.take<double>(np + 1);
+        unsigned *flags = cv.take<unsigned>(1);
+        UL_HIP(hipMemsetAsync(flags, 0, sizeof(unsigned), s));
+        UL_HIP(ul::launch_fuzzy_graph(n, k, knn_ids, knn_dists, rows, cols, vals, rho, sigma, partial, np, flags, s));
+        unsigned hflags = 0;
+        UL_HIP(hipMemcpyAsync(&hflags, flags, sizeof hflags, hipMemcpyDeviceToHost, s));
+        UL_HIP(hipFreeAsync(scratch, s));
+        scratch = nullptr;
+        UL_HIP(hipStreamSynchronize(s));
+        if (hflags & ul::kBadIndex) return fail(UMAP_E_INVAL, "a neighbour id is outside [0, n)");
+        if (hflags & ul::kBadValue) return fail(UMAP_E_INVAL, "a neighbour distance is not finite");
+        return UMAP_OK;
+    } catch (const HipFailure &f) {
+        if (scratch) hipFreeAsync(scratch, s);
+        return hip_fail(f);
+    }
+}
+
+int umap_probe_copy(const void *src, void *dst, int64_t bytes, void *stream)
+{
+    if (!src || !dst || bytes < 0 || bytes % 16) return fail(UMAP_E_INVAL, "need non-NULL pointers and bytes % 16 == 0");
+    try {
+        UL_HIP(ul::launch_probe_copy(src, dst, bytes, static_cast<hipStream_t>(stream)));
+        return UMAP_OK;
+    } catch (const HipFailure &f) {
+        return hip_fail(f);
+    }
+}
+
+}  // extern "C"

@@ -1,0 +1,314 @@
+// kernels_prep.hip -- device ingest of the COO graph B (sparse-data handling
+// section: the COO list is sorted by row and indexed by a CSR row pointer).
+//
+// Steps (all on the handle's stream, one host synchronisation at the end):
+//   1. check indices and values; w_max = largest weight of a candidate edge
+//      (val > 0, row != col)
+//   2. count kept edges per row (candidates with val >= w_max / n_epochs)
+//   3. exclusive scan of the counts -> row_ptr (int64), largest row
+//   4. scatter kept edges into their row's segment (order inside a row is
+//      arbitrary at this point)
+//   5. sort each row by column with a rank sort (the rank of an entry is the
+//      number of smaller columns in its row; equal columns flag a duplicate),
+//      and compute eps = w_max / val
+//   6. symmetry: each kept (i, j, v) must find (j, i) with bit-equal v by
+//      binary search in row j
+//   7. wave partition for the epoch kernel
+#include "internal.hpp"
+
+namespace ul {
+
+constexpr int kScanThreads = 256;
+constexpr int kScanItems = 8;
+constexpr int kScanTile = kScanThreads * kScanItems;
+
+__device__ __forceinline__ bool candidate(int32_t r, int32_t c, float v, uint32_t n)
+{
+    return (uint32_t)r < n && (uint32_t)c < n && r != c && v > 0.0f && isfinite(v);
+}
+
+__device__ __forceinline__ float keep_threshold(const PrepScalars *S, int32_t n_epochs)
+{
+    return __uint_as_float(S->wmax_bits) / (float)n_epochs;
+}
+
+__device__ __forceinline__ unsigned wave_or(unsigned v)
+{
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v |= __shfl_xor(v, off);
+    return v;
+}
+
+__device__ __forceinline__ unsigned wave_max(unsigned v)
+{
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v = max(v, (unsigned)__shfl_xor(v, off));
+    return v;
+}
+
+__global__ __launch_bounds__(256) void k_check_max(const int32_t *__restrict__ rows, const int32_t *__restrict__ cols,
+                                                   const float *__restrict__ vals, int64_t nnz, uint32_t n,
+                                                   PrepScalars *S)
+{
+    unsigned flags = 0, mx = 0;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < nnz; t += stride) {
+        int32_t r = rows[t], c = cols[t];
+        float v = vals[t];
+        if ((uint32_t)r >= n || (uint32_t)c >= n) flags |= kBadIndex;
+        if (!isfinite(v)) flags |= kBadValue;
+        if (candidate(r, c, v, n)) mx = max(mx, __float_as_uint(v));  // positive floats order as integers
+    }
+    flags = wave_or(flags);
+    mx = wave_max(mx);
+    if ((threadIdx.x & 63) == 0) {
+        if (flags) atomicOr(&S->flags, flags);
+        if (mx) atomicMax(&S->wmax_bits, mx);
+    }
+}
+
+__global__ __launch_bounds__(256) void k_count(const int32_t *__restrict__ rows, const int32_t *__restrict__ cols,
+                                               const float *__restrict__ vals, int64_t nnz, uint32_t n,
+                                               int32_t n_epochs, const PrepScalars *S, int32_t *__restrict__ deg)
+{
+    const float thresh = keep_threshold(S, n_epochs);
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < nnz; t += stride) {
+        int32_t r = rows[t], c = cols[t];
+        float v = vals[t];
+        if (candidate(r, c, v, n) && v >= thresh) atomicAdd(&deg[r], 1);
+    }
+}
+
+// Inclusive scan of one value per thread across a 256-thread block.
+__device__ __forceinline__ int64_t block_inclusive_scan(int64_t x, int64_t *s_wave)
+{
+    const unsigned lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        int64_t y = __shfl_up(x, off);
+        if (lane >= (unsigned)off) x += y;
+    }
+    if (lane == 63) s_wave[wv] = x;
+    __syncthreads();
+    int64_t add = 0;
+    for (unsigned k = 0; k < wv; ++k) add += s_wave[k];
+    __syncthreads();
+    return x + add;
+}
+
+__global__ __launch_bounds__(kScanThreads) void k_scan_reduce(const int32_t *__restrict__ deg, int64_t n,
+                                                              int64_t *__restrict__ bsum, PrepScalars *S)
+{
+    const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
+    int64_t s = 0;
+    int mx = 0;
+#pragma unroll
+    for (int k = 0; k < kScanItems; ++k)
+        if (base + k < n) {
+            int v = deg[base + k];
+            s += v;
+            mx = max(mx, v);
+        }
+    __shared__ int64_t s_wave[4];
+    int64_t inc = block_inclusive_scan(s, s_wave);
+    if (threadIdx.x == kScanThreads - 1) bsum[blockIdx.x] = inc;
+    mx = (int)wave_max((unsigned)mx);
+    if ((threadIdx.x & 63) == 0 && mx) atomicMax(&S->max_degree, mx);
+}
+
+// Exclusive scan of the block sums in place (one block, loops over chunks).
+__global__ __launch_bounds__(kScanThreads) void k_scan_top(int64_t *__restrict__ bsum, int64_t nb)
+{
+    __shared__ int64_t s_wave[4];
+    __shared__ int64_t s_carry;
+    if (threadIdx.x == 0) s_carry = 0;
+    __syncthreads();
+    for (int64_t base = 0; base < nb; base += kScanThreads) {
+        int64_t t = base + threadIdx.x;
+        int64_t v = t < nb ? bsum[t] : 0;
+        int64_t inc = block_inclusive_scan(v, s_wave);
+        int64_t carry = s_carry;
+        if (t < nb) bsum[t] = carry + inc - v;
+        __syncthreads();
+        if (threadIdx.x == kScanThreads - 1) s_carry = carry + inc;
+        __syncthreads();
+    }
+}
+
+__global__ __launch_bounds__(kScanThreads) void k_scan_down(const int32_t *__restrict__ deg, int64_t n,
+                                                            const int64_t *__restrict__ boff,
+                                                            int64_t *__restrict__ row_ptr, int64_t nb)
+{
+    const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
+    int v[kScanItems];
+    int64_t s = 0;
+#pragma unroll
+    for (int k = 0; k < kScanItems; ++k) {
+        v[k] = base + k < n ? deg[base + k] : 0;
+        s += v[k];
+    }
+    __shared__ int64_t s_wave[4];
+    int64_t run = block_inclusive_scan(s, s_wave) - s + boff[blockIdx.x];
+#pragma unroll
+    for (int k = 0; k < kScanItems; ++k)
+        if (base + k < n) {
+            row_ptr[base + k] = run;
+            run += v[k];
+        }
+    // the last block also writes the total
+    if (blockIdx.x == nb - 1 && threadIdx.x == kScanThreads - 1) row_ptr[n] = run;
+}
+
+__global__ __launch_bounds__(256) void k_scatter(const int32_t *__restrict__ rows, const int32_t *__restrict__ cols,
+                                                 const float *__restrict__ vals, int64_t nnz, uint32_t n,
+                                                 int32_t n_epochs, const PrepScalars *S,
+                                                 const int64_t *__restrict__ row_ptr, int32_t *__restrict__ cursor,
+                                                 int32_t *__restrict__ trow, int32_t *__restrict__ tcol,
+                                                 float *__restrict__ tval)
+{
+    const float thresh = keep_threshold(S, n_epochs);
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < nnz; t += stride) {
+        int32_t r = rows[t], c = cols[t];
+        float v = vals[t];
+        if (candidate(r, c, v, n) && v >= thresh) {
+            int64_t p = row_ptr[r] + atomicAdd(&cursor[r], 1);
+            trow[p] = r;
+            tcol[p] = c;
+            tval[p] = v;
+        }
+    }
+}
+
+__global__ __launch_bounds__(256) void k_row_sort(const int32_t *__restrict__ trow, const int32_t *__restrict__ tcol,
+                                                  const float *__restrict__ tval, const int64_t *__restrict__ row_ptr,
+                                                  int64_t n, PrepScalars *S, int32_t *__restrict__ col,
+                                                  float *__restrict__ sval, float *__restrict__ eps)
+{
+    const int64_t kept = row_ptr[n];
+    const float w_max = __uint_as_float(S->wmax_bits);
+    unsigned flags = 0;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < kept; p += stride) {
+        const int32_t r = trow[p];
+        const int32_t c = tcol[p];
+        const int64_t rs = row_ptr[r], re = row_ptr[r + 1];
+        int64_t rank = 0;
+        for (int64_t q = rs; q < re; ++q) {
+            int32_t cq = tcol[q];
+            rank += cq < c;
+            if (cq == c && q != p) flags |= kDuplicate;
+        }
+        const int64_t dst = rs + rank;
+        const float v = tval[p];
+        col[dst] = c;
+        sval[dst] = v;
+        eps[dst] = w_max / v;
+    }
+    flags = wave_or(flags);
+    if ((threadIdx.x & 63) == 0 && flags) atomicOr(&S->flags, flags);
+}
+
+__global__ __launch_bounds__(256) void k_symmetry(const int32_t *__restrict__ trow, const int32_t *__restrict__ col,
+                                                  const float *__restrict__ sval, const int64_t *__restrict__ row_ptr,
+                                                  int64_t n, PrepScalars *S)
+{
+    // After a duplicate the in-row sort leaves some slots unwritten; the
+    // graph is rejected anyway, so skip the check rather than read them.
+    if (S->flags & (kDuplicate | kBadIndex | kBadValue)) return;
+    const int64_t kept = row_ptr[n];
+    unsigned flags = 0;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < kept; p += stride) {
+        const int32_t i = trow[p];   // row slots keep their row through the in-row sort
+        const int32_t j = col[p];
+        if ((uint32_t)j >= (uint32_t)n) {
+            flags |= kAsymmetric;
+            continue;
+        }
+        int64_t lo = row_ptr[j], hi = row_ptr[j + 1];
+        const int64_t end = hi;
+        while (lo < hi) {
+            int64_t mid = (lo + hi) >> 1;
+            if (col[mid] < i) lo = mid + 1; else hi = mid;
+        }
+        if (lo >= end || col[lo] != i || __float_as_uint(sval[lo]) != __float_as_uint(sval[p])) flags |= kAsymmetric;
+    }
+    flags = wave_or(flags);
+    if ((threadIdx.x & 63) == 0 && flags) atomicOr(&S->flags, flags);
+}
+
+static int64_t grid_for(int64_t items)
+{
+    int64_t b = (items + 255) / 256;
+    if (b > 256 * 32) b = 256 * 32;
+    return b < 1 ? 1 : b;
+}
+
+int64_t scan_blocks(int64_t n) { return (n + kScanTile - 1) / kScanTile; }
+
+hipError_t launch_prep(const PrepBuffers &B, hipStream_t s)
+{
+    const uint32_t n = (uint32_t)B.n;
+    const int64_t g = grid_for(B.nnz);
+    hipLaunchKernelGGL(k_check_max, dim3((unsigned)g), dim3(256), 0, s, B.rows, B.cols, B.vals, B.nnz, n, B.scalars);
+    hipLaunchKernelGGL(k_count, dim3((unsigned)g), dim3(256), 0, s, B.rows, B.cols, B.vals, B.nnz, n, B.n_epochs,
+                       B.scalars, B.deg);
+    const int64_t nb = B.nblocks_scan;
+    hipLaunchKernelGGL(k_scan_reduce, dim3((unsigned)nb), dim3(kScanThreads), 0, s, B.deg, B.n, B.bsum, B.scalars);
+    hipLaunchKernelGGL(k_scan_top, dim3(1), dim3(kScanThreads), 0, s, B.bsum, nb);
+    hipLaunchKernelGGL(k_scan_down, dim3((unsigned)nb), dim3(kScanThreads), 0, s, B.deg, B.n, B.bsum, B.row_ptr, nb);
+    hipLaunchKernelGGL(k_scatter, dim3((unsigned)g), dim3(256), 0, s, B.rows, B.cols, B.vals, B.nnz, n, B.n_epochs,
+                       B.scalars, B.row_ptr, B.cursor, B.trow, B.tcol, B.tval);
+    hipLaunchKernelGGL(k_row_sort, dim3((unsigned)g), dim3(256), 0, s, B.trow, B.tcol, B.tval, B.row_ptr, B.n,
+                       B.scalars, B.col, B.sval, B.eps);
+    hipLaunchKernelGGL(k_symmetry, dim3((unsigned)g), dim3(256), 0, s, B.trow, B.col, B.sval, B.row_ptr, B.n,
+                       B.scalars);
+    return hipGetLastError();
+}
+
+// part[w] = first row r with row_ptr[r] + wgt * r >= w * kWaveCost, for
+// w < n_waves; part[n_waves] = n.  A wave then holds at most rows_cap(dim)
+// rows (cost rises by >= wgt per row) and about kWaveCost edges unless its
+// last row alone is longer.
+__global__ void k_partition(const int64_t *__restrict__ row_ptr, int64_t n, int32_t wgt, int32_t *__restrict__ part,
+                            int64_t n_waves)
+{
+    const int64_t w = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (w > n_waves) return;
+    if (w == n_waves) {
+        part[w] = (int32_t)n;
+        return;
+    }
+    const int64_t target = w * (int64_t)kWaveCost;
+    int64_t lo = 0, hi = n;
+    while (lo < hi) {
+        int64_t mid = (lo + hi) >> 1;
+        if (row_ptr[mid] + (int64_t)wgt * mid >= target) hi = mid; else lo = mid + 1;
+    }
+    part[w] = (int32_t)lo;
+}
+
+hipError_t launch_partition(const int64_t *row_ptr, int64_t n, int32_t dim, int32_t *part, int64_t n_waves,
+                            hipStream_t s)
+{
+    int64_t blocks = (n_waves + 1 + 255) / 256;
+    hipLaunchKernelGGL(k_partition, dim3((unsigned)blocks), dim3(256), 0, s, row_ptr, n, row_weight(dim), part,
+                       n_waves);
+    return hipGetLastError();
+}
+
+__global__ void k_zero_u64(unsigned long long *p, int64_t count)
+{
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < count; t += stride) p[t] = 0;
+}
+
+hipError_t launch_zero_u64(unsigned long long *p, int64_t count, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_zero_u64, dim3((unsigned)grid_for(count)), dim3(256), 0, s, p, count);
+    return hipGetLastError();
+}
+
+}  // namespace ul

@@ -1,0 +1,127 @@
+"""C-ABI boundary checks that need no GPU: the library loads, exports every
+function its header declares, and rejects invalid arguments before any HIP
+call (status codes and messages)."""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2008_00325_amd import umap_layout as U
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "umap_layout.h")
+
+
+@pytest.fixture(scope="module")
+def L():
+    return U.lib()
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(umap_\w+)\s*\(", text)))
+
+
+def test_every_declared_function_is_exported(L):
+    names = _declared()
+    assert len(names) == 18
+    for name in names:
+        assert hasattr(L, name), name
+        assert name in U.EXPORTS
+    assert sorted(U.EXPORTS) == names
+
+
+def test_status_codes_match_header():
+    text = open(HEADER).read()
+    codes = dict((m, int(v)) for m, v in re.findall(r"#define (UMAP_\w+) \(?(-?\d+)\)?", text))
+    for name, value in codes.items():
+        assert getattr(U, name) == value
+
+
+def _create(n=4, dim=2, rows=(0, 1), cols=(1, 0), vals=(1.0, 1.0), a=1.5, b=0.9, N=10, R=5):
+    return U.umap_layout_create(n, dim, np.array(rows), np.array(cols), np.array(vals), a, b, N, R)
+
+
+@pytest.mark.parametrize("kw,frag", [
+    (dict(n=0), "n must be"),
+    (dict(n=2**31), "n must be"),
+    (dict(dim=0), "n_components"),
+    (dict(dim=17), "n_components"),
+    (dict(a=0.0), "a must be"),
+    (dict(a=float("nan")), "a must be"),
+    (dict(b=-1.0), "b must be"),
+    (dict(b=float("inf")), "b must be"),
+    (dict(N=0), "n_epochs"),
+    (dict(N=2**24), "n_epochs"),
+    (dict(R=-1), "neg_rate"),
+    (dict(R=2**16), "neg_rate"),
+    (dict(rows=(0, 4)), "outside"),
+    (dict(cols=(-1, 0)), "outside"),
+    (dict(vals=(1.0, float("nan"))), "not finite"),
+    (dict(vals=(float("inf"), 1.0)), "not finite"),
+])
+def test_create_rejects_invalid_arguments(kw, frag):
+    with pytest.raises(U.UmapLayoutError) as ei:
+        _create(**kw)
+    assert ei.value.code == U.UMAP_E_INVAL
+    assert frag in U.umap_layout_last_error()
+
+
+def test_create_device_rejects_scalars_without_touching_the_gpu(L):
+    out = ctypes.c_void_p(123)
+    rc = L.umap_layout_create_device(ctypes.byref(out), 10, 0, None, None, None, 0, 1.0, 1.0, 10, 5, None)
+    assert rc == U.UMAP_E_INVAL and out.value is None
+    rc = L.umap_layout_create_device(ctypes.byref(out), 10, 2, None, None, None, 5, 1.0, 1.0, 10, 5, None)
+    assert rc == U.UMAP_E_INVAL and "NULL" in U.umap_layout_last_error()
+    assert L.umap_layout_create(None, 10, 2, None, None, None, 0, 1.0, 1.0, 10, 5) == U.UMAP_E_INVAL
+
+
+def test_null_handles_are_rejected(L):
+    assert L.umap_layout_run(None, 1) == U.UMAP_E_INVAL
+    assert L.umap_layout_run_epochs(None, 1, 0, 1) == U.UMAP_E_INVAL
+    assert L.umap_layout_get(None, None) == U.UMAP_E_INVAL
+    assert L.umap_layout_get_device(None, None) == U.UMAP_E_INVAL
+    assert L.umap_layout_set_embedding(None, None) == U.UMAP_E_INVAL
+    assert L.umap_layout_get_graph(None, None, None, None, None) == U.UMAP_E_INVAL
+    assert L.umap_layout_stats(None, None) == U.UMAP_E_INVAL
+    assert L.umap_layout_set_stream(None, None) == U.UMAP_E_INVAL
+    assert L.umap_layout_set_kernel(None, 0) == U.UMAP_E_INVAL
+    assert L.umap_layout_debug_active(None, 0, None) == U.UMAP_E_INVAL
+    assert L.umap_layout_debug_negatives(None, 0, 0, 0, 0, None) == U.UMAP_E_INVAL
+    L.umap_layout_destroy(None)  # no-op
+
+
+def test_fuzzy_graph_and_probe_argument_checks(L):
+    p = ctypes.c_void_p(16)
+    assert L.umap_fuzzy_graph_device(0, 15, p, p, p, p, p, None) == U.UMAP_E_INVAL
+    assert L.umap_fuzzy_graph_device(10, 0, p, p, p, p, p, None) == U.UMAP_E_INVAL
+    assert L.umap_fuzzy_graph_device(10, 1025, p, p, p, p, p, None) == U.UMAP_E_INVAL
+    assert L.umap_fuzzy_graph_device(2**30, 2, p, p, p, p, p, None) == U.UMAP_E_INVAL
+    assert L.umap_fuzzy_graph_device(10, 5, None, p, p, p, p, None) == U.UMAP_E_INVAL
+    assert L.umap_probe_copy(p, p, 17, None) == U.UMAP_E_INVAL
+    assert L.umap_probe_copy(None, p, 16, None) == U.UMAP_E_INVAL
+
+
+def test_fit_ab_matches_oracle(orc):
+    for spread, md in [(1.0, 0.1), (1.0, 0.5), (2.0, 0.05), (0.5, 0.0)]:
+        a, b = U.umap_fit_ab(spread, md)
+        ra, rb = orc.fit_ab(spread, md)
+        assert abs(a - ra) < 1e-5 * ra and abs(b - rb) < 1e-5 * rb
+    with pytest.raises(U.UmapLayoutError):
+        U.umap_fit_ab(0.0, 0.1)
+    with pytest.raises(U.UmapLayoutError):
+        U.umap_fit_ab(1.0, 3.5)
+
+
+def test_create_without_a_gpu_reports_device_error():
+    import torch
+
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present")
+    with pytest.raises(U.UmapLayoutError) as ei:
+        _create()
+    assert ei.value.code == U.UMAP_E_DEVICE

@@ -1,0 +1,367 @@
+"""GPU parity of the layout path against the CPU oracle (MI355X, gfx950).
+
+Every test goes through the C ABI (ctypes binding) and compares with the
+oracle on the same seeded inputs:
+  * the ingested graph (row_ptr, col, eps): bit-exact;
+  * the schedule (active edges per epoch) and the negative-sample draws:
+    bit-exact;
+  * the random initial layout: bit-exact;
+  * one epoch fed the same fp32 state: max |GPU - oracle| <= 1e-4;
+  * a full run: trustworthiness at k = 15 within 0.01 of the oracle's run;
+  * determinism, resume and the two epoch kernels: bit-identical.
+"""
+
+import sys
+
+import numpy as np
+import pytest
+
+import oracle as O
+from paper_2008_00325_amd import synth
+from paper_2008_00325_amd import umap_layout as U
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-4
+A_DEF, B_DEF = 1.5769434, 0.8950608
+
+
+def case(msg):
+    print(f"[gpu case] {msg}", flush=True)
+    sys.stdout.flush()
+
+
+def _coo_from_knn(ids, dist):
+    return O.fuzzy_graph(ids, dist)
+
+
+@pytest.fixture(scope="module")
+def blobs_graph():
+    w = synth.WORKLOADS["blobs2k"]
+    X, _ = synth.workload_points(w)
+    ids, dist = O.exact_knn(X, w.k)
+    r, c, v = _coo_from_knn(ids, dist)
+    return w, X, ids, dist, (r, c, v)
+
+
+@pytest.fixture(scope="module")
+def window1m_graph():
+    w = synth.WORKLOADS["window1m"]
+    ids, dist = synth.workload_knn(w)
+    r, c, v = _coo_from_knn(ids, dist)
+    return w, ids, dist, (r, c, v)
+
+
+def _shuffled(coo, seed):
+    r, c, v = coo
+    p = np.random.default_rng(seed).permutation(r.size)
+    return r[p], c[p], v[p]
+
+
+def _check_graph(h, g):
+    row_ptr, col, eps = U.umap_layout_get_graph(h)
+    assert np.array_equal(row_ptr, g.row_ptr)
+    assert np.array_equal(col, g.col)
+    assert np.array_equal(eps.view(np.uint32), g.eps.view(np.uint32))
+    st = U.umap_layout_stats(h)
+    assert st["nnz_kept"] == g.nnz and np.float32(st["w_max"]) == np.float32(g.w_max)
+
+
+# ---------------------------------------------------------------------------
+# ingest
+# ---------------------------------------------------------------------------
+
+def test_graph_bit_exact_host_and_device(blobs_graph):
+    import torch
+
+    w, X, ids, dist, coo = blobs_graph
+    r, c, v = _shuffled(coo, 1)
+    # zeros, negatives and self loops must be dropped
+    r = np.concatenate([r, [3, 4, 5]]).astype(np.int32)
+    c = np.concatenate([c, [3, 9, 6]]).astype(np.int32)
+    v = np.concatenate([v, [0.7, 0.0, -1.0]]).astype(np.float32)
+    g = O.prep(w.n, r, c, v, w.n_epochs)
+    case("graph blobs2k host create")
+    with U.umap_layout_create(w.n, 2, r, c, v, A_DEF, B_DEF, w.n_epochs, 5) as h:
+        _check_graph(h, g)
+    case("graph blobs2k device create")
+    dr, dc, dv = (torch.from_numpy(x).cuda() for x in (r, c, v))
+    with U.umap_layout_create_device(w.n, 2, dr, dc, dv, r.size, A_DEF, B_DEF, w.n_epochs, 5) as h:
+        _check_graph(h, g)
+
+
+@pytest.mark.parametrize("n,deg,N", [(1, 0, 10), (7, 3, 1), (3001, 9, 200), (20011, 30, 50)])
+def test_graph_bit_exact_random(n, deg, N):
+    if deg == 0:
+        r = c = np.zeros(0, np.int32)
+        v = np.zeros(0, np.float32)
+    else:
+        r, c, v = synth.random_symmetric_coo(n, deg, seed=n)
+    g = O.prep(n, r, c, v, N)
+    case(f"graph random n={n} deg={deg} N={N}")
+    with U.umap_layout_create(n, 3, r, c, v, A_DEF, B_DEF, N, 5) as h:
+        _check_graph(h, g)
+
+
+def test_graph_hub_row():
+    # a star: vertex 0 joined to every other vertex (a row of n-1 edges)
+    n = 6000
+    others = np.arange(1, n, dtype=np.int32)
+    vals = np.random.default_rng(3).random(n - 1).astype(np.float32) + np.float32(0.01)
+    r = np.concatenate([np.zeros(n - 1, np.int32), others])
+    c = np.concatenate([others, np.zeros(n - 1, np.int32)])
+    v = np.concatenate([vals, vals])
+    r, c, v = _shuffled((r, c, v), 2)
+    g = O.prep(n, r, c, v, 100)
+    case("graph star n=6000")
+    with U.umap_layout_create(n, 2, r, c, v, A_DEF, B_DEF, 100, 5) as h:
+        _check_graph(h, g)
+        E = synth.embedding_state(n, 2, 9)
+        for ep in (0, 50, 99):
+            U.umap_layout_set_embedding(h, E)
+            U.umap_layout_run_epochs(h, 4, ep, ep + 1)
+            ref, act = O.epoch(g, E, ep, A_DEF, B_DEF, 100, 5, 4)
+            assert np.abs(U.umap_layout_get(h) - ref).max() <= TOL
+            assert U.umap_layout_stats(h)["active_edges"] == act
+
+
+def test_graph_errors_on_device():
+    import torch
+
+    r = np.array([0, 1, 1, 2], np.int32)
+    c = np.array([1, 0, 2, 1], np.int32)
+    case("asymmetric value")
+    with pytest.raises(U.UmapLayoutError) as ei:
+        U.umap_layout_create(3, 2, r, c, np.float32([0.5, 0.5, 0.5, 0.25]), A_DEF, B_DEF, 10, 5)
+    assert ei.value.code == U.UMAP_E_ASYMMETRIC
+    case("missing reverse edge")
+    with pytest.raises(U.UmapLayoutError) as ei:
+        U.umap_layout_create(3, 2, r[:3], c[:3], np.float32([0.5, 0.5, 0.5]), A_DEF, B_DEF, 10, 5)
+    assert ei.value.code == U.UMAP_E_ASYMMETRIC
+    case("duplicate edge")
+    with pytest.raises(U.UmapLayoutError) as ei:
+        U.umap_layout_create(3, 2, np.r_[r, 0], np.r_[c, 1], np.float32([0.5] * 5), A_DEF, B_DEF, 10, 5)
+    assert ei.value.code == U.UMAP_E_INVAL and "more than once" in U.umap_layout_last_error()
+    case("device path: index out of range and non-finite value")
+    for rr, vv, frag in [(np.int32([0, 1, 1, 7]), np.float32([0.5] * 4), "outside"),
+                         (r, np.float32([0.5, np.nan, 0.5, 0.5]), "not finite")]:
+        dr, dc, dv = (torch.from_numpy(x).cuda() for x in (rr, c, vv))
+        with pytest.raises(U.UmapLayoutError) as ei:
+            U.umap_layout_create_device(3, 2, dr, dc, dv, 4, A_DEF, B_DEF, 10, 5)
+        assert ei.value.code == U.UMAP_E_INVAL and frag in U.umap_layout_last_error()
+
+
+# ---------------------------------------------------------------------------
+# schedule, random streams, initial layout
+# ---------------------------------------------------------------------------
+
+def test_active_mask_and_negatives_bit_exact(blobs_graph):
+    w, X, ids, dist, (r, c, v) = blobs_graph
+    g = O.prep(w.n, r, c, v, w.n_epochs)
+    case("active mask / negatives blobs2k")
+    with U.umap_layout_create(w.n, 2, r, c, v, A_DEF, B_DEF, w.n_epochs, 5) as h:
+        for ep in (0, 1, 2, 3, w.n_epochs // 2, w.n_epochs - 1):
+            assert np.array_equal(U.umap_layout_debug_active(h, ep), O.active_mask(g.eps, ep))
+        for seed, ep, e0 in [(0, 0, 0), (2**40 + 7, 17, 1234), (2**64 - 1, w.n_epochs - 1, g.nnz - 500)]:
+            got = U.umap_layout_debug_negatives(h, seed, ep, e0, 500)
+            ref = O.negative_vertices(seed, ep, e0, 500, 5, w.n)
+            assert np.array_equal(got, ref)
+
+
+@pytest.mark.parametrize("n,dim", [(1, 1), (1000, 2), (4097, 3), (3000, 16)])
+def test_init_bit_exact(n, dim):
+    case(f"init n={n} dim={dim}")
+    empty = np.zeros(0, np.int32)
+    with U.umap_layout_create(n, dim, empty, empty, np.zeros(0, np.float32), A_DEF, B_DEF, 3, 5) as h:
+        for seed in (0, 12345, 2**63 + 5):
+            U.umap_layout_run(h, seed)
+            assert np.array_equal(U.umap_layout_get(h).view(np.uint32), O.init_layout(n, dim, seed).view(np.uint32))
+            assert U.umap_layout_stats(h)["active_edges"] == 0
+
+
+# ---------------------------------------------------------------------------
+# one epoch from the same state
+# ---------------------------------------------------------------------------
+
+def _epoch_parity(h, g, E, epochs, a, b, N, R, seed, label):
+    for ep in epochs:
+        case(f"{label} epoch {ep}")
+        U.umap_layout_set_embedding(h, E)
+        U.umap_layout_run_epochs(h, seed, ep, ep + 1)
+        got = U.umap_layout_get(h)
+        ref, act = O.epoch(g, E, ep, a, b, N, R, seed)
+        err = float(np.abs(got.astype(np.float64) - ref).max())
+        print(f"  max|diff| = {err:.3e}  active = {act}", flush=True)
+        assert err <= TOL
+        assert U.umap_layout_stats(h)["active_edges"] == act
+
+
+def test_single_epoch_blobs(blobs_graph):
+    w, X, ids, dist, (r, c, v) = blobs_graph
+    g = O.prep(w.n, r, c, v, w.n_epochs)
+    a, b = O.fit_ab(w.spread, w.min_dist)
+    # the oracle's own trajectory, rounded to fp32, as the fed states
+    E0 = O.init_layout(w.n, 2, 7).astype(np.float64)
+    states = [E0]
+    E = E0
+    for ep in range(30):
+        E, _ = O.epoch(g, E, ep, a, b, w.n_epochs, w.neg_rate, 7)
+    states.append(E)
+    with U.umap_layout_create(w.n, 2, r, c, v, a, b, w.n_epochs, w.neg_rate) as h:
+        for kernel in (0, 1):
+            U.umap_layout_set_kernel(h, kernel)
+            for s in states:
+                _epoch_parity(h, g, s.astype(np.float32), (0, 1, w.n_epochs // 2, w.n_epochs - 1), a, b,
+                              w.n_epochs, w.neg_rate, 7, f"blobs2k kernel {kernel}")
+
+
+def test_single_epoch_window1m_full_size(window1m_graph):
+    """The workload the benchmark times (1M vertices, k = 15, 2-D), whole
+    layout compared, in the benchmark's launch configuration."""
+    import torch
+
+    w, ids, dist, (r, c, v) = window1m_graph
+    g = O.prep(w.n, r, c, v, w.n_epochs)
+    a, b = O.fit_ab(w.spread, w.min_dist)
+    dr, dc, dv = (torch.from_numpy(x).cuda() for x in (r, c, v))
+    with U.umap_layout_create_device(w.n, w.dim, dr, dc, dv, r.size, a, b, w.n_epochs, w.neg_rate) as h:
+        _check_graph(h, g)
+        for scale, seed in ((10.0, 3), (0.5, 4)):
+            E = synth.embedding_state(w.n, w.dim, seed, scale)
+            _epoch_parity(h, g, E, (0, 1, w.n_epochs // 2, w.n_epochs - 1), a, b, w.n_epochs, w.neg_rate, 11,
+                          f"window1m scale {scale}")
+
+
+@pytest.mark.parametrize("dim,R,N", [(1, 5, 20), (3, 5, 200), (4, 0, 50), (16, 7, 30)])
+def test_single_epoch_dims_and_rates(dim, R, N):
+    n = 5003
+    bounds = synth.cluster_bounds(n, 3)
+    ids, dist = synth.window_knn(n, 15, bounds, seed=dim)
+    r, c, v = O.fuzzy_graph(ids, dist)
+    g = O.prep(n, r, c, v, N)
+    with U.umap_layout_create(n, dim, r, c, v, A_DEF, B_DEF, N, R) as h:
+        for kernel in (0, 1):
+            U.umap_layout_set_kernel(h, kernel)
+            for scale in (10.0, 0.3):
+                E = synth.embedding_state(n, dim, dim + 100, scale)
+                _epoch_parity(h, g, E, (0, 1, N // 2, N - 1), A_DEF, B_DEF, N, R, 5,
+                              f"dim {dim} R {R} kernel {kernel} scale {scale}")
+
+
+# ---------------------------------------------------------------------------
+# whole runs
+# ---------------------------------------------------------------------------
+
+def test_kernels_bit_identical_and_deterministic(window1m_graph):
+    w, ids, dist, (r, c, v) = window1m_graph
+    sub = (r < 200_000) & (c < 200_000)
+    r, c, v = r[sub], c[sub], v[sub]
+    n = 200_000
+    N = 20
+    case("two kernels and two runs, 200k vertices, 20 epochs")
+    with U.umap_layout_create(n, 2, r, c, v, A_DEF, B_DEF, N, 5) as h:
+        U.umap_layout_run(h, 77)
+        first = U.umap_layout_get(h)
+        U.umap_layout_run(h, 77)
+        assert np.array_equal(U.umap_layout_get(h).view(np.uint32), first.view(np.uint32))
+        U.umap_layout_set_kernel(h, 1)
+        U.umap_layout_run(h, 77)
+        assert np.array_equal(U.umap_layout_get(h).view(np.uint32), first.view(np.uint32))
+        U.umap_layout_set_kernel(h, 0)
+        U.umap_layout_run(h, 78)
+        assert not np.array_equal(U.umap_layout_get(h), first)
+
+
+def test_resume_equals_uninterrupted(blobs_graph):
+    w, X, ids, dist, (r, c, v) = blobs_graph
+    N = 60
+    case("resume at epoch 23 of 60")
+    with U.umap_layout_create(w.n, 2, r, c, v, A_DEF, B_DEF, N, 5) as h:
+        U.umap_layout_run(h, 5)
+        full = U.umap_layout_get(h)
+        U.umap_layout_set_embedding(h, O.init_layout(w.n, 2, 5))
+        U.umap_layout_run_epochs(h, 5, 0, 23)
+        mid = U.umap_layout_get(h)
+    with U.umap_layout_create(w.n, 2, r, c, v, A_DEF, B_DEF, N, 5) as h2:
+        U.umap_layout_set_embedding(h2, mid)
+        U.umap_layout_run_epochs(h2, 5, 23, N)
+        assert np.array_equal(U.umap_layout_get(h2).view(np.uint32), full.view(np.uint32))
+
+
+def test_full_run_trustworthiness(blobs_graph):
+    w, X, ids, dist, (r, c, v) = blobs_graph
+    g = O.prep(w.n, r, c, v, w.n_epochs)
+    a, b = O.fit_ab(w.spread, w.min_dist)
+    for seed in (0, 1):
+        case(f"full run blobs2k seed {seed}")
+        with U.umap_layout_create(w.n, w.dim, r, c, v, a, b, w.n_epochs, w.neg_rate) as h:
+            U.umap_layout_run(h, seed)
+            Eg = U.umap_layout_get(h)
+            st = U.umap_layout_stats(h)
+        Eo, act = O.run(g, w.dim, a, b, w.n_epochs, w.neg_rate, seed)
+        assert st["active_edges"] == int(act.sum())
+        assert st["edge_updates"] == int(act.sum()) * (1 + w.neg_rate)
+        tg = O.trustworthiness(X, Eg, 15)
+        to = O.trustworthiness(X, Eo, 15)
+        print(f"  T(gpu) = {tg:.5f}  T(oracle) = {to:.5f}", flush=True)
+        assert abs(tg - to) <= 0.01
+        assert np.all(np.isfinite(Eg))
+
+
+def test_fault_injection(monkeypatch, blobs_graph):
+    w, X, ids, dist, (r, c, v) = blobs_graph
+    case("fault injection")
+    monkeypatch.setenv("UMAP_LAYOUT_FAULT", "alloc")
+    with pytest.raises(U.UmapLayoutError) as ei:
+        U.umap_layout_create(w.n, 2, r, c, v, A_DEF, B_DEF, 10, 5)
+    assert ei.value.code == U.UMAP_E_NOMEM
+    monkeypatch.setenv("UMAP_LAYOUT_FAULT", "launch@3")
+    with U.umap_layout_create(w.n, 2, r, c, v, A_DEF, B_DEF, 10, 5) as h:
+        with pytest.raises(U.UmapLayoutError) as ei:
+            U.umap_layout_run(h, 1)
+        assert ei.value.code == U.UMAP_E_DEVICE
+        monkeypatch.delenv("UMAP_LAYOUT_FAULT")
+        U.umap_layout_run(h, 1)
+        assert np.all(np.isfinite(U.umap_layout_get(h)))
+    with U.umap_layout_create(w.n, 2, r, c, v, A_DEF, B_DEF, 10, 5) as h:
+        with pytest.raises(U.UmapLayoutError) as ei:
+            U.umap_layout_run_epochs(h, 1, 0, 1)
+        assert ei.value.code == U.UMAP_E_STATE
+
+
+# ---------------------------------------------------------------------------
+# input side: kNN lists -> B on the device
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("which", ["blobs2k", "window"])
+def test_fuzzy_graph_device(which, blobs_graph):
+    import torch
+
+    if which == "blobs2k":
+        w, X, ids, dist, _ = blobs_graph
+        n, k = w.n, w.k
+    else:
+        n, k = 30011, 30
+        ids, dist = synth.window_knn(n, k, synth.cluster_bounds(n, 7), seed=13)
+    case(f"fuzzy graph {which}")
+    di = torch.from_numpy(np.ascontiguousarray(ids)).cuda()
+    dd = torch.from_numpy(np.ascontiguousarray(dist)).cuda()
+    rows = torch.empty(2 * n * k, dtype=torch.int32, device="cuda")
+    cols = torch.empty_like(rows)
+    vals = torch.empty(2 * n * k, dtype=torch.float32, device="cuda")
+    U.umap_fuzzy_graph_device(n, k, di, dd, rows, cols, vals)
+    torch.cuda.synchronize()
+    rg, cg, vg = rows.cpu().numpy(), cols.cpu().numpy(), vals.cpu().numpy()
+    keep = (vg > 0) & (rg != cg)
+    order = np.lexsort((cg[keep], rg[keep]))
+    rg, cg, vg = rg[keep][order], cg[keep][order], vg[keep][order]
+    ro, co, vo = O.fuzzy_union(ids, O.membership(dist, *O.smooth_knn(dist)))
+    assert np.array_equal(rg, ro) and np.array_equal(cg, co)
+    ulp = np.abs(vg.view(np.int32).astype(np.int64) - vo.astype(np.float32).view(np.int32).astype(np.int64))
+    assert ulp.max() <= 1
+    # and it ingests into the same graph as the oracle's union (up to those ulps)
+    with U.umap_layout_create_device(n, 2, rows, cols, vals, 2 * n * k, A_DEF, B_DEF, 200, 5) as h:
+        row_ptr, col, eps = U.umap_layout_get_graph(h)
+    g = O.prep(n, ro, co, vo.astype(np.float32), 200)
+    assert np.array_equal(row_ptr, g.row_ptr) and np.array_equal(col, g.col)
+    assert np.allclose(eps, g.eps, rtol=1e-6, atol=0)
