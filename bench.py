@@ -1,0 +1,249 @@
+"""Benchmark of the MI355X layout SGD (one GPU).
+
+One step = one pass of the whole layout path over the resident graph B of the
+1M-vertex workload (k = 15 window kNN, 2-D, 200 epochs, 5 negatives per
+sampled edge): device ingest (drop / prune / sort / CSR / eps / symmetry
+check), random initialisation, the 200 epoch kernels and the device-to-device
+copy of the result.  B is built on the GPU from the seeded kNN lists before the
+timed region.
+
+value = edge-updates (sampled edges + drawn negatives, over all epochs of all
+timed steps) / wall time of the timed steps.  The 200-epoch layout time, the
+ingest time and the epoch kernel's roofline come from the library's HIP events
+on the stream the kernels run on.  The CPU baseline times the C oracle on a
+bounded sample of epochs of the same workload.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+Prints one JSON line on stdout.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "epoch_traffic_window1m.json")
+KERNEL_SOURCES = ["paper_2008_00325_amd/csrc/kernels_layout.hip", "paper_2008_00325_amd/csrc/layout_device.hpp"]
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def kernel_hash() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def algorithmic_bytes_per_epoch(n: int, dim: int, nnz: int, active: float, neg_rate: int) -> float:
+    """Bytes one epoch must move at least (pull form, fp32 / int32): eps of every
+    kept edge, col of each sampled edge, row_ptr + read y_i + write y_i' per
+    vertex, and one dim-vector gather per positive sample and per negative."""
+    return 4.0 * nnz + 4.0 * active + (4.0 + 8.0 * dim) * n + 4.0 * dim * active + 4.0 * dim * neg_rate * active
+
+
+def build_input(w, torch, U):
+    from paper_2008_00325_amd import synth
+
+    t0 = time.time()
+    ids, dist = synth.workload_knn(w)
+    log(f"generated kNN lists {ids.shape} in {time.time() - t0:.1f}s")
+    n, k = w.n, w.k
+    di = torch.from_numpy(ids).cuda()
+    dd = torch.from_numpy(dist).cuda()
+    rows = torch.empty(2 * n * k, dtype=torch.int32, device="cuda")
+    cols = torch.empty_like(rows)
+    vals = torch.empty(2 * n * k, dtype=torch.float32, device="cuda")
+    U.umap_fuzzy_graph_device(n, k, di, dd, rows, cols, vals)
+    torch.cuda.synchronize()
+    del di, dd
+    a, b = U.umap_fit_ab(w.spread, w.min_dist)
+    return ids, dist, rows, cols, vals, a, b
+
+
+def gpu_steps(w, torch, U, coo, a, b, steps: int, warmup: int):
+    rows, cols, vals = coo
+    nnz = rows.numel()
+    out = torch.empty((w.n, w.dim), dtype=torch.float32, device="cuda")
+
+    def one_step(seed):
+        with U.umap_layout_create_device(w.n, w.dim, rows, cols, vals, nnz, a, b, w.n_epochs, w.neg_rate) as h:
+            U.umap_layout_run(h, seed)
+            U.umap_layout_get_device(h, out)
+            st = U.umap_layout_stats(h)
+        return st
+
+    for s in range(warmup):
+        st = one_step(1000 + s)
+        log(f"warmup step {s}: epochs {st['epochs_ms']:.2f} ms, ingest {st['prep_ms']:.2f} ms")
+    torch.cuda.synchronize()
+    stats = []
+    t0 = time.perf_counter()
+    for s in range(steps):
+        stats.append(one_step(s))
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    for s, st in enumerate(stats):
+        log(f"step {s}: epochs {st['epochs_ms']:.2f} ms, init {st['init_ms']:.3f} ms, ingest {st['prep_ms']:.2f} ms, "
+            f"{st['edge_updates']} edge updates")
+    ok = bool(torch.isfinite(out).all().item())
+    return stats, wall, ok
+
+
+def copy_probe(torch, U, mb: int = 1024, reps: int = 5) -> float:
+    """HBM copy bandwidth of the library's plain 16-byte copy kernel (GB/s,
+    read + write bytes), on the current stream."""
+    nbytes = mb * 1024 * 1024
+    src = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    stream = torch.cuda.current_stream()
+    U.umap_probe_copy(src, dst, nbytes, stream)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        U.umap_probe_copy(src, dst, nbytes, stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    return 2.0 * nbytes / (ms * 1e-3) / 1e9
+
+
+def cpu_baseline(w, ids, dist, budget_s: float = 20.0):
+    """The C oracle (fp64 push-form Jacobi epochs) timed on the host cores, on
+    a sample of epochs spread over the run, from the random initial layout."""
+    import oracle as O
+
+    t0 = time.time()
+    r, c, v = O.fuzzy_graph(ids, dist)
+    g = O.prep(w.n, r, c, v, w.n_epochs)
+    a, b = O.fit_ab(w.spread, w.min_dist)
+    E = O.init_layout(w.n, w.dim, 0).astype(np.float64)
+    log(f"oracle graph ready in {time.time() - t0:.1f}s ({g.nnz} edges); timing epochs")
+    sample = [0, 100, 199, 50, 150, 25, 75, 125, 175]
+    done, updates, spent = [], 0, 0.0
+    for ep in sample:
+        t1 = time.perf_counter()
+        _, act = O.epoch(g, E, ep, a, b, w.n_epochs, w.neg_rate, 0)
+        spent += time.perf_counter() - t1
+        updates += act * (1 + w.neg_rate)
+        done.append(ep)
+        if spent > budget_s:
+            break
+    return {
+        "value": updates / spent,
+        "unit": "edge-updates/s",
+        "cores": O.num_threads(),
+        "kind": "oracle",
+        "sample": f"epochs {done} of the {w.n_epochs}-epoch {w.name} layout from the random initial layout "
+                  f"(fp64 push form, {updates} edge updates in {spent:.2f} s)",
+    }
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="window1m")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (the layout is measured on a single MI355X); got --gpus {args.gpus}",
+              file=sys.stderr)
+        return 2
+
+    import torch
+
+    from paper_2008_00325_amd import synth
+    from paper_2008_00325_amd import umap_layout as U
+
+    U.lib()
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 2
+    torch.cuda.set_device(0)
+    w = synth.WORKLOADS[args.workload]
+    ids, dist, rows, cols, vals, a, b = build_input(w, torch, U)
+    stats, wall, finite = gpu_steps(w, torch, U, (rows, cols, vals), a, b, args.steps, args.warmup)
+    if not finite:
+        log("non-finite layout")
+        return 1
+    updates = sum(s["edge_updates"] for s in stats)
+    st = stats[-1]
+    epochs_ms = float(np.median([s["epochs_ms"] for s in stats]))
+    prep_ms = float(np.median([s["prep_ms"] for s in stats]))
+    init_ms = float(np.median([s["init_ms"] for s in stats]))
+    n_epochs = st["n_epochs"]
+    avg_active = st["active_edges"] / n_epochs
+    bytes_epoch = algorithmic_bytes_per_epoch(w.n, w.dim, st["nnz_kept"], avg_active, w.neg_rate)
+    launch_ms = epochs_ms / n_epochs
+    achieved = bytes_epoch / (launch_ms * 1e-3) / 1e9
+    traffic = None
+    if os.path.exists(PROFILE_TRAFFIC):
+        with open(PROFILE_TRAFFIC) as f:
+            prof = json.load(f)
+        if prof.get("kernel_hash") == kernel_hash() and prof.get("workload") == w.name:
+            traffic = prof.get("bytes_per_launch")
+    copy_gbps = copy_probe(torch, U)
+    gpu_name = torch.cuda.get_device_name(0)
+
+    result = {
+        "metric": "SGD edge-updates/sec (pos+neg) and 200-epoch layout wall time at 1M points",
+        "value": updates / wall,
+        "unit": "edge-updates/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": wall / args.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": w.name, "n": w.n, "k": w.k, "n_components": w.dim, "n_epochs": w.n_epochs,
+            "neg_rate": w.neg_rate, "min_dist": w.min_dist, "spread": w.spread, "a": a, "b": b,
+            "nnz_input": st["nnz_input"], "nnz_kept": st["nnz_kept"], "max_degree": st["max_degree"],
+            "step": "device ingest + init + all epochs + device copy-out",
+        },
+        "layout_wall_s": epochs_ms * 1e-3,
+        "layout_epochs_updates_per_s": st["edge_updates"] / (epochs_ms * 1e-3),
+        "ingest_ms": prep_ms,
+        "init_ms": init_ms,
+        "edge_updates_per_step": st["edge_updates"],
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "k_epoch_wave<2>",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBPS,
+            "traffic": traffic,
+            "algorithmic_bytes_per_launch": bytes_epoch,
+            "avg_launch_ms": launch_ms,
+        },
+        "hbm_copy_probe_GBps": copy_gbps,
+        "gpu": gpu_name,
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(w, ids, dist)
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

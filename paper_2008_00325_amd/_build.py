@@ -19,6 +19,8 @@ HIPCC_FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     # IEEE fp32 division: the edge schedule is a floor of a quotient
     "-fhip-fp32-correctly-rounded-divide-sqrt",
+    # no implicit fma contraction: every kernel variant rounds identically
+    "-ffp-contract=off",
     "-Wall", "-Wno-unused-command-line-argument",
 ]
 

@@ -14,7 +14,7 @@
 #include <string>
 #include <vector>
 
-#include "../../include/umap_layout.h"
+#include "umap_layout.h"
 #include "internal.hpp"
 
 namespace {
@@ -124,10 +124,20 @@ struct umap_layout {
     float *eps = nullptr;
     int32_t *part = nullptr;
     int64_t n_waves = 0;
+    uint8_t *head = nullptr;       // edge's row relative to its wave's first row
+    int32_t *act_edge = nullptr;   // per-epoch scratch list of sampled edges
+    int32_t *act_tail = nullptr;
+    uint8_t *act_head = nullptr;
     float *E[2] = {nullptr, nullptr};
     int cur = 0;
     bool has_layout = false;
-    unsigned long long *active = nullptr;   // n_epochs counters
+    unsigned long long *active = nullptr;   // n_epochs sampled-edge counts
+    int32_t *counts = nullptr;              // ring of per-wave counts
+    int32_t lg_phases = 0;                  // negative samples split over 2^lg table ranges
+    uint32_t *rec = nullptr;                // records of negative samples, per range
+    int32_t *rec_count = nullptr;           // per range and wave
+    long long *delta = nullptr;             // fixed-point partial sums between launches
+    int64_t count_stride = 0;               // slots per ring row
     hipEvent_t ev[3] = {nullptr, nullptr, nullptr};
     umap_layout_stats_t st{};
 
@@ -171,8 +181,16 @@ int create_common(umap_layout **out, int64_t n, int32_t dim, const int32_t *rows
         const int wgt = ul::row_weight(dim);
         const int64_t max_waves = (nnz + (int64_t)wgt * n) / ul::kWaveCost + 2;
         const size_t nd = (size_t)n * (size_t)dim;
+        const int64_t count_stride =
+            ul::count_slots(1, n, 0) > max_waves ? ul::count_slots(1, n, 0) : max_waves;
+        const int64_t count_rows = n_epochs < ul::kCountRing ? n_epochs : ul::kCountRing;
+        const int32_t lg_phases = ul::phase_log2(n, dim);
+        const int64_t n_phases = (int64_t)1 << lg_phases;
         size_t bytes = need<int64_t>(n + 1) + need<int32_t>(nnz) + need<float>(nnz) + need<int32_t>(max_waves + 1) +
-                       2 * need<float>(nd) + need<unsigned long long>(n_epochs);
+                       2 * need<float>(nd) + need<unsigned long long>(n_epochs) + 2 * need<uint8_t>(nnz) +
+                       2 * need<int32_t>(nnz) + need<int32_t>((size_t)count_rows * count_stride) +
+                       need<uint32_t>((size_t)n_phases * neg_rate * nnz) + need<int32_t>((size_t)n_phases * max_waves) +
+                       need<long long>(nd);
         if (fault_alloc()) throw HipFailure{hipErrorOutOfMemory, "hipMalloc(arena) [injected]"};
         UL_HIP(hipMalloc(&h->arena, bytes));
         Carver cv{static_cast<char *>(h->arena)};
@@ -183,6 +201,16 @@ int create_common(umap_layout **out, int64_t n, int32_t dim, const int32_t *rows
         h->E[0] = cv.take<float>(nd);
         h->E[1] = cv.take<float>(nd);
         h->active = cv.take<unsigned long long>(n_epochs);
+        h->head = cv.take<uint8_t>(nnz);
+        h->act_edge = cv.take<int32_t>(nnz);
+        h->act_tail = cv.take<int32_t>(nnz);
+        h->act_head = cv.take<uint8_t>(nnz);
+        h->counts = cv.take<int32_t>((size_t)count_rows * count_stride);
+        h->count_stride = count_stride;
+        h->lg_phases = lg_phases;
+        h->rec = cv.take<uint32_t>((size_t)n_phases * neg_rate * nnz);
+        h->rec_count = cv.take<int32_t>((size_t)n_phases * max_waves);
+        h->delta = cv.take<long long>(nd);
 
         // ingest scratch (stream-ordered)
         ul::PrepBuffers B{};
@@ -256,7 +284,7 @@ int create_common(umap_layout **out, int64_t n, int32_t dim, const int32_t *rows
         memcpy(&h->w_max, &S.wmax_bits, sizeof(float));
         h->n_waves = (kept + (int64_t)wgt * n + ul::kWaveCost - 1) / ul::kWaveCost;
         if (h->n_waves < 1) h->n_waves = 1;
-        UL_HIP(ul::launch_partition(h->row_ptr, n, dim, h->part, h->n_waves, stream));
+        UL_HIP(ul::launch_partition(h->row_ptr, n, dim, h->part, h->n_waves, h->head, stream));
         float ms = 0;
         UL_HIP(hipEventElapsedTime(&ms, h->ev[0], h->ev[1]));
         h->st.prep_ms = ms;
@@ -286,8 +314,17 @@ int run_epochs_impl(umap_layout *h, uint64_t seed, int32_t first, int32_t last, 
     A.b = h->b;
     A.key_lo = (uint32_t)seed;
     A.key_hi = (uint32_t)(seed >> 32);
+    ul::WaveGraph G{h->row_ptr, h->col,      h->eps,      h->head,     h->part,
+                    h->n_waves,  h->act_edge, h->act_tail, h->act_head, 1 << h->lg_phases,
+                    h->lg_phases, h->rec,     (int64_t)h->neg_rate * h->nnz, h->rec_count, h->delta};
     UL_HIP(ul::launch_zero_u64(h->active, h->n_epochs, h->stream));
     UL_HIP(hipEventRecord(h->ev[1], h->stream));
+    // the wave kernels store a sample's offset inside its table range in 24
+    // bits; beyond that (n >= 2^28 vertices) the one-thread-per-vertex kernel runs
+    const int kernel = ((h->n >> h->lg_phases) + 2 < ((int64_t)1 << 24)) ? h->kernel : 1;
+    const int64_t slots = ul::count_slots(kernel, h->n, h->n_waves);
+    const int ring = h->n_epochs < ul::kCountRing ? h->n_epochs : ul::kCountRing;
+    int32_t pending_from = first;   // first epoch whose counts are not yet summed
     for (int32_t ep = first; ep < last; ++ep) {
         if (ep == fault) {
             UL_HIP(hipStreamSynchronize(h->stream));
@@ -297,9 +334,14 @@ int run_epochs_impl(umap_layout *h, uint64_t seed, int32_t first, int32_t last, 
         A.E_next = h->E[1 - h->cur];
         A.epoch = ep;
         A.alpha = 1.0 - (double)ep / (double)h->n_epochs;
-        A.active_count = h->active + ep;
-        UL_HIP(ul::launch_epoch(h->kernel, h->dim, A, h->row_ptr, h->col, h->eps, h->part, h->n_waves, h->stream));
+        A.counts = h->counts + (int64_t)((ep - pending_from) % ring) * h->count_stride;
+        UL_HIP(ul::launch_epoch(kernel, h->dim, A, G, h->stream));
         h->cur = 1 - h->cur;
+        if (ep + 1 - pending_from == ring || ep + 1 == last) {
+            UL_HIP(ul::launch_reduce_counts(h->counts, h->count_stride, slots, ep + 1 - pending_from,
+                                            h->active + pending_from, h->stream));
+            pending_from = ep + 1;
+        }
     }
     UL_HIP(hipEventRecord(h->ev[2], h->stream));
     std::vector<unsigned long long> act((size_t)h->n_epochs);

@@ -4,7 +4,7 @@
 // with step halving on 300 points of [0, 3 spread].
 #include <math.h>
 
-#include "../../include/umap_layout.h"
+#include "umap_layout.h"
 #include "internal.hpp"
 
 namespace {

@@ -28,10 +28,12 @@ struct PrepScalars {
 };
 
 // Work split of the wavefront epoch kernel: wave w owns the whole rows
-// [part[w], part[w+1]); consecutive waves cover about kWaveCost units of
-// (edges + row_weight * rows).
-constexpr int kWaveCost = 512;
-__host__ __device__ constexpr int row_weight(int dim) { return dim > 2 ? dim : 2; }
+// [part[w], part[w+1]), chosen so that consecutive waves cover about
+// kWaveCost units of (edges + row_weight * rows).  The row weight bounds the
+// rows of a wave (and so its LDS accumulator) by rows_cap; long waves amortise
+// the per-wave set-up and commit.
+constexpr int kWaveCost = 8192;
+__host__ __device__ constexpr int row_weight(int dim) { return 32 * (dim > 2 ? dim : 2); }
 __host__ __device__ constexpr int rows_cap(int dim) { return kWaveCost / row_weight(dim) + 1; }
 
 // ---- ingest (kernels_prep.hip) ----
@@ -62,13 +64,47 @@ struct PrepBuffers {
 int64_t scan_blocks(int64_t n);
 hipError_t launch_prep(const PrepBuffers &B, hipStream_t s);
 hipError_t launch_partition(const int64_t *row_ptr, int64_t n, int32_t dim, int32_t *part, int64_t n_waves,
-                            hipStream_t s);
+                            uint8_t *head, hipStream_t s);
 hipError_t launch_zero_u64(unsigned long long *p, int64_t count, hipStream_t s);
 
 // ---- layout (kernels_layout.hip) ----
 hipError_t launch_init(float *E, int64_t n, int32_t dim, uint64_t seed, hipStream_t s);
-hipError_t launch_epoch(int kernel, int32_t dim, const EpochArgs &A, const int64_t *row_ptr, const int32_t *col,
-                        const float *eps, const int32_t *part, int64_t n_waves, hipStream_t s);
+// Graph-side arrays of the epoch kernels.
+struct WaveGraph {
+    const int64_t *row_ptr;   // n + 1
+    const int32_t *col;       // kept edges, sorted by (row, col)
+    const float *eps;         // epochs per sample of each edge
+    const uint8_t *head;      // row of each edge relative to its wave's first row
+    const int32_t *part;      // n_waves + 1 wave boundaries (rows)
+    int64_t n_waves;
+    int32_t *act_edge;        // scratch: sampled edges of the epoch, per wave slice
+    int32_t *act_tail;
+    uint8_t *act_head;
+    // negative samples are filed by vertex-table range: P = 2^lg_phases ranges
+    int32_t n_phases;
+    int32_t lg_phases;
+    uint32_t *rec;            // P x rec_stride records ((row in wave) << 24 | offset in range)
+    int64_t rec_stride;       // neg_rate x kept edges: wave w's slice starts at neg_rate x e0
+    int32_t *rec_count;       // P x n_waves
+    long long *delta;         // n x dim fixed-point partial sums between launches
+};
+
+// At most this many table ranges (phases) per epoch.
+constexpr int kMaxPhases = 16;
+// Table bytes per range: small enough to stay resident in one XCD's 4 MB L2
+// next to the streamed edge data.
+constexpr int64_t kPhaseTableBytes = 2 << 20;
+// log2 of the number of ranges for a table of n vertices x dim.
+int32_t phase_log2(int64_t n, int32_t dim);
+
+hipError_t launch_epoch(int kernel, int32_t dim, const EpochArgs &A, const WaveGraph &G, hipStream_t s);
+// Count slots one epoch of `kernel` writes (one per wave).
+int64_t count_slots(int kernel, int64_t n, int64_t n_waves);
+// out[r] = sum of counts[r * stride + 0 .. slots) for r < rows.
+hipError_t launch_reduce_counts(const int32_t *counts, int64_t stride, int64_t slots, int32_t rows,
+                                unsigned long long *out, hipStream_t s);
+// Epochs whose per-wave counts are kept before they are summed.
+constexpr int kCountRing = 256;
 hipError_t launch_debug_active(const float *eps, int64_t nnz, int32_t epoch, uint8_t *out, hipStream_t s);
 hipError_t launch_debug_negatives(uint32_t n, uint64_t seed, int32_t epoch, int64_t e_first, int64_t count,
                                   int32_t neg_rate, uint32_t *out, hipStream_t s);

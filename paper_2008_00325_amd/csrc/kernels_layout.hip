@@ -6,9 +6,9 @@
 // accumulator, and E_{n+1} = E_n + alpha * sum is written to the other buffer
 // (no scatter to global memory, no global atomics on the embedding).
 //  * k_epoch_wave:    edge-parallel.  Each wavefront owns a range of whole rows
-//                     (balanced by edges + rows).  It streams the rows' eps in
-//                     64-edge chunks, compacts the sampled edges into an LDS
-//                     queue, and runs full 64-lane batches in which each lane
+//                     (balanced by edges + rows).  It streams the rows' eps,
+//                     compacts the sampled edges into its slice of a scratch
+//                     list, then runs full 64-lane batches in which each lane
 //                     handles one sampled edge: its attraction and its
 //                     negative samples.  Sums go to a per-wave LDS accumulator
 //                     with 64-bit integer atomics; the wave then writes its
@@ -55,9 +55,9 @@ hipError_t launch_init(float *E, int64_t n, int32_t dim, uint64_t seed, hipStrea
 }
 
 // ---------------------------------------------------------------------------
-// One thread per vertex.
+// One thread per vertex: the whole epoch for its row, term by term.
 // ---------------------------------------------------------------------------
-template <int DIM>
+template <int DIM, int NQ>
 __global__ __launch_bounds__(256) void k_epoch_rowwise(EpochArgs A, const int64_t *__restrict__ row_ptr,
                                                        const int32_t *__restrict__ col,
                                                        const float *__restrict__ eps)
@@ -66,144 +66,367 @@ __global__ __launch_bounds__(256) void k_epoch_rowwise(EpochArgs A, const int64_
     unsigned long long cnt = 0;
     if (i < A.n) {
         float yi[DIM];
-#pragma unroll
-        for (int d = 0; d < DIM; ++d) yi[d] = A.E[(size_t)i * DIM + d];
+        load_row<DIM>(A.E, i, yi);
         long long acc[DIM];
 #pragma unroll
         for (int d = 0; d < DIM; ++d) acc[d] = 0;
         const int64_t e1 = row_ptr[i + 1];
         for (int64_t e = row_ptr[i]; e < e1; ++e) {
             if (!edge_active(eps[e], A.epoch)) continue;
+            ++cnt;
+            float yj[DIM];
+            load_row<DIM>(A.E, (uint32_t)col[e], yj);
             long long fx[DIM];
-            edge_contribution<DIM>(A, e, i, (uint32_t)col[e], yi, fx);
+            attraction_fixed<DIM>(yi, yj, A.a, A.b, fx);
 #pragma unroll
             for (int d = 0; d < DIM; ++d) acc[d] += fx[d];
-            ++cnt;
+            for (int32_t q = 0; 4 * q < A.neg_rate; ++q) {
+                Ctr w = negative_words(e, A.epoch, q, A.key_lo, A.key_hi);
+                for (int t = 0; t < 4 && 4 * q + t < A.neg_rate; ++t) {
+                    const uint32_t k = word_to_vertex(t == 0 ? w.w[0] : t == 1 ? w.w[1] : t == 2 ? w.w[2] : w.w[3],
+                                                      A.n);
+                    if (k == i) continue;
+                    float yk[DIM];
+                    load_row<DIM>(A.E, k, yk);
+                    repulsion_fixed<DIM>(yi, yk, A.a, A.b, fx);
+#pragma unroll
+                    for (int d = 0; d < DIM; ++d) acc[d] += fx[d];
+                }
+            }
         }
 #pragma unroll
         for (int d = 0; d < DIM; ++d) A.E_next[(size_t)i * DIM + d] = commit(yi[d], acc[d], A.alpha);
     }
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) cnt += __shfl_xor(cnt, off);
-    if ((threadIdx.x & 63) == 0 && cnt) atomicAdd(A.active_count, cnt);
+    if ((threadIdx.x & 63) == 0) A.counts[blockIdx.x * 4 + threadIdx.x / 64] = (int32_t)cnt;
 }
 
 // ---------------------------------------------------------------------------
-// Edge-parallel wavefront kernel.
+// Edge-parallel wavefront kernels.
+//
+// Each wave owns the whole rows [part[w], part[w+1]).  An epoch is one
+// k_epoch_draw launch followed by P k_epoch_repulse launches:
+//  * k_epoch_draw streams eps (and col, and each edge's row inside the wave)
+//    over the wave's edges, classifies every edge for this epoch and appends
+//    the sampled ones -- compacted with a ballot -- to the wave's slice of a
+//    scratch list.  It then takes the list 64 edges at a time: each lane adds
+//    its edge's attraction to the wave's LDS accumulator, draws the edge's
+//    negative samples and files each one as a 4-byte record under the range
+//    of the vertex table it falls in.  The accumulator goes to delta.
+//  * k_epoch_repulse (range p) reads the wave's records of range p and adds
+//    their repulsions.  All gathers of one launch hit one 1/P slice of the
+//    vertex table, which is sized to stay resident in an XCD's L2.  The last
+//    range commits the wave's rows of E_{n+1} with coalesced stores.
 // ---------------------------------------------------------------------------
 constexpr int kWavesPerBlock = 4;
+// The eps / col / head stream is read in super-chunks of kSuper x 64 edges,
+// double buffered in registers: super-chunk s+1 is in flight while s is
+// classified.
+constexpr int kSuper = 4;
+// Records per lane per step of the repulsion kernel.
+constexpr int kRepUnroll = 8;
 
-// One batch: lane l handles queued edge q (if `valid`).  The head row is
-// found by binary search in the wave's LDS copy of row_ptr.
-template <int DIM>
-__device__ __forceinline__ void wave_batch(const EpochArgs &A, const int32_t *__restrict__ col,
-                                           const int64_t *rp, int nrows, int64_t r0, int64_t e0,
-                                           long long *acc, int32_t off, bool valid)
+__device__ __forceinline__ int64_t uniform64(int64_t v)
 {
-    if (!valid) return;
-    const int64_t e = e0 + off;
-    int lo = 0, hi = nrows - 1;   // largest h with rp[h] <= e
-    while (lo < hi) {
-        int mid = (lo + hi + 1) >> 1;
-        if (rp[mid] <= e) lo = mid; else hi = mid - 1;
-    }
-    const uint32_t i = (uint32_t)(r0 + lo);
-    float yi[DIM];
-#pragma unroll
-    for (int d = 0; d < DIM; ++d) yi[d] = A.E[(size_t)i * DIM + d];
-    long long fx[DIM];
-    edge_contribution<DIM>(A, e, i, (uint32_t)col[e], yi, fx);
-#pragma unroll
-    for (int d = 0; d < DIM; ++d)
-        atomicAdd(reinterpret_cast<unsigned long long *>(&acc[lo * DIM + d]), (unsigned long long)fx[d]);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)(uint64_t)v);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)v >> 32));
+    return (int64_t)(((uint64_t)hi << 32) | lo);
 }
 
-template <int DIM>
-__global__ __launch_bounds__(256) void k_epoch_wave(EpochArgs A, const int64_t *__restrict__ row_ptr,
-                                                    const int32_t *__restrict__ col,
-                                                    const float *__restrict__ eps,
-                                                    const int32_t *__restrict__ part, int64_t n_waves)
+// Logical wave index of this lane's wave.  Workgroups are dispatched
+// round-robin over the 8 XCDs; each XCD gets a contiguous run of logical
+// blocks so that neighbouring rows (and their mostly-local neighbours) share
+// one L2.
+__device__ __forceinline__ int64_t logical_wave()
+{
+    const int64_t per_xcd = gridDim.x / 8;
+    const int64_t lb = (int64_t)(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+    return lb * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+}
+
+// first vertex of table range p of P = 2^lg (ranges split the 32-bit draw)
+__device__ __forceinline__ uint32_t range_base(uint32_t p, int32_t lg, uint32_t n)
+{
+    return lg == 0 ? 0u : __umulhi(p << (32 - lg), n);
+}
+
+template <int DIM, int NQ>
+__global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
 {
     constexpr int CAP = rows_cap(DIM);
     __shared__ long long s_acc[kWavesPerBlock][CAP * DIM];
-    __shared__ int64_t s_rp[kWavesPerBlock][CAP + 1];
-    __shared__ int32_t s_q[kWavesPerBlock][2 * kWave];
+    __shared__ float s_y[kWavesPerBlock][CAP * DIM];   // the wave's own rows of E_n
+    __shared__ uint32_t s_rec[kWavesPerBlock][kMaxPhases];
 
-    // Workgroups are dispatched round-robin over the 8 XCDs; give each XCD a
-    // contiguous run of logical blocks so that neighbouring rows (and their
-    // mostly-local neighbours) share one L2.
-    const int64_t per_xcd = gridDim.x / 8;
-    const int64_t lb = (int64_t)(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
-    const int wv = threadIdx.x / kWave;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const unsigned lane = threadIdx.x % kWave;
-    const int64_t w = lb * kWavesPerBlock + wv;
-    if (w >= n_waves) return;
-    const int64_t r0 = part[w];
-    const int nrows = (int)(part[w + 1] - r0);
-    if (nrows <= 0) return;
+    const int64_t w = logical_wave();
+    if (w >= G.n_waves) return;
+    const int64_t r0 = __builtin_amdgcn_readfirstlane(G.part[w]);
+    const int nrows = __builtin_amdgcn_readfirstlane(G.part[w + 1]) - (int)r0;
+    if (nrows <= 0) {
+        if (lane == 0) A.counts[w] = 0;
+        if ((int)lane < G.n_phases) G.rec_count[(int64_t)lane * G.n_waves + w] = 0;
+        return;
+    }
+    const int64_t e0 = uniform64(G.row_ptr[r0]);
+    const int64_t e1 = uniform64(G.row_ptr[r0 + nrows]);
 
     long long *acc = s_acc[wv];
-    int64_t *rp = s_rp[wv];
-    int32_t *q = s_q[wv];
-    for (int t = lane; t <= nrows; t += kWave) rp[t] = row_ptr[r0 + t];
-    for (int t = lane; t < nrows * DIM; t += kWave) acc[t] = 0;
-    wave_sync();
+    float *yrows = s_y[wv];
+    uint32_t *rec_n = s_rec[wv];
+    const size_t g0 = (size_t)r0 * DIM;
+    for (int t = lane; t < nrows * DIM; t += kWave) {
+        acc[t] = 0;
+        yrows[t] = A.E[g0 + t];
+    }
+    if ((int)lane < kMaxPhases) rec_n[lane] = 0;
 
-    const int64_t e0 = rp[0], e1 = rp[nrows];
-    int qn = 0;
-    unsigned long long cnt = 0;
-    for (int64_t base = e0; base < e1; base += kWave) {
-        const int64_t e = base + lane;
-        const bool act = e < e1 && edge_active(eps[e], A.epoch);
-        const unsigned long long m = __ballot(act);
-        if (act) q[qn + lanes_below(m)] = (int32_t)(e - e0);
-        const int c = __popcll(m);
-        qn += c;
-        cnt += c;
-        wave_sync();
-        if (qn >= kWave) {
-            wave_batch<DIM>(A, col, rp, nrows, r0, e0, acc, q[lane], true);
-            wave_sync();
-            if ((int)lane < qn - kWave) q[lane] = q[kWave + lane];
-            qn -= kWave;
-            wave_sync();
+    // ---- classify and compact ----------------------------------------------
+    int64_t qn = 0;
+    // loads are unconditional (the index is clamped into the wave's range and
+    // the value masked) so that the next super-chunk stays in flight
+    auto load_super = [&](int64_t sbase, float (&ev)[kSuper], int32_t (&cv)[kSuper], uint8_t (&hv)[kSuper]) {
+#pragma unroll
+        for (int j = 0; j < kSuper; ++j) {
+            int64_t e = sbase + j * kWave + lane;
+            e = e < e1 ? e : e1 - 1;
+            ev[j] = G.eps[e];
+            cv[j] = G.col[e];
+            hv[j] = G.head[e];
+        }
+    };
+    auto scan_super = [&](int64_t sbase, const float (&ev)[kSuper], const int32_t (&cv)[kSuper],
+                          const uint8_t (&hv)[kSuper]) {
+#pragma unroll
+        for (int j = 0; j < kSuper; ++j) {
+            const int64_t e = sbase + j * kWave + lane;
+            if (sbase + j * kWave >= e1) break;
+            const bool act = edge_active(ev[j], A.epoch) & (e < e1);
+            const unsigned long long m = __ballot(act);
+            if (act) {
+                const int64_t pos = e0 + qn + lanes_below(m);
+                G.act_edge[pos] = (int32_t)e;
+                G.act_tail[pos] = cv[j];
+                G.act_head[pos] = hv[j];
+            }
+            qn += __popcll(m);
+        }
+    };
+    if (e1 > e0) {
+        float ea[kSuper], eb[kSuper];
+        int32_t ca[kSuper], cb[kSuper];
+        uint8_t ha[kSuper], hb[kSuper];
+        constexpr int64_t kStep = (int64_t)kSuper * kWave;
+        load_super(e0, ea, ca, ha);
+        for (int64_t s0 = e0; s0 < e1; s0 += 2 * kStep) {
+            load_super(s0 + kStep, eb, cb, hb);
+            scan_super(s0, ea, ca, ha);
+            if (s0 + kStep >= e1) break;
+            load_super(s0 + 2 * kStep, ea, ca, ha);
+            scan_super(s0 + kStep, eb, cb, hb);
         }
     }
-    if (qn > 0) wave_batch<DIM>(A, col, rp, nrows, r0, e0, acc, q[lane], (int)lane < qn);
+    // the list written by this wave's lanes is read back by other lanes of
+    // the same wave (same CU)
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+
+    // ---- attraction + negative draws, 64 sampled edges per batch ------------
+    const int32_t R = A.neg_rate;
+    const int32_t lg = G.lg_phases;
+    uint32_t *const rec_wave = G.rec + (int64_t)R * e0;   // this wave's slice of every range
+    auto file = [&](uint32_t u, uint32_t i, int h) {
+        const uint32_t k = word_to_vertex(u, A.n);
+        if (k == i) return;   // a draw equal to the source adds nothing
+        const uint32_t p = lg == 0 ? 0u : u >> (32 - lg);
+        const uint32_t slot = atomicAdd(&rec_n[p], 1u);
+        rec_wave[(int64_t)p * G.rec_stride + slot] = ((uint32_t)h << 24) | (k - range_base(p, lg, A.n));
+    };
+    for (int64_t b = 0; b < qn; b += kWave) {
+        const bool valid = b + lane < qn;
+        const int64_t slot = valid ? e0 + b + lane : e0;
+        const int64_t e = G.act_edge[slot];
+        const uint32_t tail = (uint32_t)G.act_tail[slot];
+        const int h = G.act_head[slot];
+        const uint32_t i = (uint32_t)(r0 + h);
+        float yi[DIM], yj[DIM];
+#pragma unroll
+        for (int d = 0; d < DIM; ++d) yi[d] = yrows[h * DIM + d];
+        load_row<DIM>(A.E, tail, yj);
+        long long fx[DIM];
+        attraction_fixed<DIM>(yi, yj, A.a, A.b, fx);
+        if (valid) {
+#pragma unroll
+            for (int d = 0; d < DIM; ++d)
+                atomicAdd(reinterpret_cast<unsigned long long *>(&acc[h * DIM + d]), (unsigned long long)fx[d]);
+            if constexpr (NQ >= 0) {
+                uint32_t u[4 * NQ > 0 ? 4 * NQ : 1];
+                if constexpr (NQ > 0) negative_words_all<NQ>(e, A.epoch, A.key_lo, A.key_hi, u);
+#pragma unroll
+                for (int r = 0; r < 4 * NQ; ++r)
+                    if (r < R) file(u[r], i, h);
+            } else {
+                for (int32_t q = 0; 4 * q < R; ++q) {
+                    Ctr wd = negative_words(e, A.epoch, q, A.key_lo, A.key_hi);
+#pragma unroll
+                    for (int t = 0; t < 4; ++t)
+                        if (4 * q + t < R) file(wd.w[t], i, h);
+                }
+            }
+        }
+    }
     wave_sync();
 
-    const size_t g0 = (size_t)r0 * DIM;
-    for (int t = lane; t < nrows * DIM; t += kWave) A.E_next[g0 + t] = commit(A.E[g0 + t], acc[t], A.alpha);
-    if (lane == 0 && cnt) atomicAdd(A.active_count, cnt);
+    for (int t = lane; t < nrows * DIM; t += kWave) G.delta[g0 + t] = acc[t];
+    if ((int)lane < G.n_phases) G.rec_count[(int64_t)lane * G.n_waves + w] = (int32_t)rec_n[lane];
+    // per-wave count, summed by a separate pass (a global atomic per wave on
+    // one address would serialise thousands of waves)
+    if (lane == 0) A.counts[w] = (int32_t)qn;
 }
 
 template <int DIM>
-static hipError_t launch_epoch_dim(int kernel, const EpochArgs &A, const int64_t *row_ptr, const int32_t *col,
-                                   const float *eps, const int32_t *part, int64_t n_waves, hipStream_t s)
+__global__ __launch_bounds__(256) void k_epoch_repulse(EpochArgs A, WaveGraph G, int32_t phase)
+{
+    constexpr int CAP = rows_cap(DIM);
+    __shared__ long long s_acc[kWavesPerBlock][CAP * DIM];
+    __shared__ float s_y[kWavesPerBlock][CAP * DIM];   // the wave's own rows of E_n
+
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const unsigned lane = threadIdx.x % kWave;
+    const int64_t w = logical_wave();
+    if (w >= G.n_waves) return;
+    const int64_t r0 = __builtin_amdgcn_readfirstlane(G.part[w]);
+    const int nrows = __builtin_amdgcn_readfirstlane(G.part[w + 1]) - (int)r0;
+    if (nrows <= 0) return;
+    const int64_t e0 = uniform64(G.row_ptr[r0]);
+    const int64_t nrec = __builtin_amdgcn_readfirstlane(G.rec_count[(int64_t)phase * G.n_waves + w]);
+    const bool last = phase + 1 == G.n_phases;
+
+    long long *acc = s_acc[wv];
+    float *yrows = s_y[wv];
+    const size_t g0 = (size_t)r0 * DIM;
+    for (int t = lane; t < nrows * DIM; t += kWave) {
+        acc[t] = G.delta[g0 + t];
+        yrows[t] = A.E[g0 + t];
+    }
+    wave_sync();
+
+    const uint32_t *recs = G.rec + (int64_t)A.neg_rate * e0 + (int64_t)phase * G.rec_stride;
+    const uint32_t base = range_base((uint32_t)phase, G.lg_phases, A.n);
+    // kRepUnroll records per lane per step, all loads issued before use
+    for (int64_t b = 0; b < nrec; b += kRepUnroll * kWave) {
+        uint32_t r[kRepUnroll];
+#pragma unroll
+        for (int u = 0; u < kRepUnroll; ++u) {
+            const int64_t t = b + u * kWave + lane;
+            r[u] = recs[t < nrec ? t : 0];
+        }
+        float yi[kRepUnroll][DIM], yk[kRepUnroll][DIM];
+#pragma unroll
+        for (int u = 0; u < kRepUnroll; ++u) load_row<DIM>(A.E, base + (r[u] & 0xFFFFFFu), yk[u]);
+#pragma unroll
+        for (int u = 0; u < kRepUnroll; ++u) {
+            const int h = (int)(r[u] >> 24);
+#pragma unroll
+            for (int d = 0; d < DIM; ++d) yi[u][d] = yrows[h * DIM + d];
+        }
+#pragma unroll
+        for (int u = 0; u < kRepUnroll; ++u) {
+            long long fx[DIM];
+            repulsion_fixed<DIM>(yi[u], yk[u], A.a, A.b, fx);
+            const int h = (int)(r[u] >> 24);
+            if (b + u * kWave + lane < nrec) {
+#pragma unroll
+                for (int d = 0; d < DIM; ++d)
+                    atomicAdd(reinterpret_cast<unsigned long long *>(&acc[h * DIM + d]), (unsigned long long)fx[d]);
+            }
+        }
+    }
+    wave_sync();
+
+    if (last) {
+        for (int t = lane; t < nrows * DIM; t += kWave) A.E_next[g0 + t] = commit(yrows[t], acc[t], A.alpha);
+    } else {
+        for (int t = lane; t < nrows * DIM; t += kWave) G.delta[g0 + t] = acc[t];
+    }
+}
+
+int32_t phase_log2(int64_t n, int32_t dim)
+{
+    const int64_t bytes = n * dim * (int64_t)sizeof(float);
+    int32_t lg = 0;
+    while ((1 << (lg + 1)) <= kMaxPhases && (bytes >> lg) > kPhaseTableBytes) ++lg;
+    return lg;
+}
+
+template <int DIM, int NQ>
+static hipError_t launch_epoch_dq(int kernel, const EpochArgs &A, const WaveGraph &G, hipStream_t s)
 {
     if (kernel == 1) {
         int64_t blocks = ((int64_t)A.n + 255) / 256;
-        hipLaunchKernelGGL(k_epoch_rowwise<DIM>, dim3((unsigned)blocks), dim3(256), 0, s, A, row_ptr, col, eps);
-    } else {
-        int64_t blocks = (n_waves + kWavesPerBlock - 1) / kWavesPerBlock;
-        int64_t per_xcd = (blocks + 7) / 8;
-        hipLaunchKernelGGL(k_epoch_wave<DIM>, dim3((unsigned)(per_xcd * 8)), dim3(256), 0, s, A, row_ptr, col, eps,
-                           part, n_waves);
+        hipLaunchKernelGGL((k_epoch_rowwise<DIM, NQ>), dim3((unsigned)blocks), dim3(256), 0, s, A, G.row_ptr, G.col,
+                           G.eps);
+        return hipGetLastError();
     }
+    const int64_t blocks = (G.n_waves + kWavesPerBlock - 1) / kWavesPerBlock;
+    const int64_t grid = ((blocks + 7) / 8) * 8;
+    hipLaunchKernelGGL((k_epoch_draw<DIM, NQ>), dim3((unsigned)grid), dim3(256), 0, s, A, G);
+    for (int32_t p = 0; p < G.n_phases; ++p)
+        hipLaunchKernelGGL((k_epoch_repulse<DIM>), dim3((unsigned)grid), dim3(256), 0, s, A, G, p);
     return hipGetLastError();
 }
 
-hipError_t launch_epoch(int kernel, int32_t dim, const EpochArgs &A, const int64_t *row_ptr, const int32_t *col,
-                        const float *eps, const int32_t *part, int64_t n_waves, hipStream_t s)
+template <int DIM>
+static hipError_t launch_epoch_dim(int kernel, const EpochArgs &A, const WaveGraph &G, hipStream_t s)
+{
+    if (A.neg_rate == 0) return launch_epoch_dq<DIM, 0>(kernel, A, G, s);
+    if (A.neg_rate <= 4) return launch_epoch_dq<DIM, 1>(kernel, A, G, s);
+    if (A.neg_rate <= 8) return launch_epoch_dq<DIM, 2>(kernel, A, G, s);
+    return launch_epoch_dq<DIM, -1>(kernel, A, G, s);
+}
+
+hipError_t launch_epoch(int kernel, int32_t dim, const EpochArgs &A, const WaveGraph &G, hipStream_t s)
 {
     switch (dim) {
 #define UL_CASE(D) \
-    case D: return launch_epoch_dim<D>(kernel, A, row_ptr, col, eps, part, n_waves, s);
+    case D: return launch_epoch_dim<D>(kernel, A, G, s);
         UL_CASE(1) UL_CASE(2) UL_CASE(3) UL_CASE(4) UL_CASE(5) UL_CASE(6) UL_CASE(7) UL_CASE(8)
         UL_CASE(9) UL_CASE(10) UL_CASE(11) UL_CASE(12) UL_CASE(13) UL_CASE(14) UL_CASE(15) UL_CASE(16)
 #undef UL_CASE
     default: return hipErrorInvalidValue;
     }
+}
+
+// ---------------------------------------------------------------------------
+// Sum of the per-wave counts of `rows` epochs: one block per epoch.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_reduce_counts(const int32_t *__restrict__ counts, int64_t stride,
+                                                       int64_t slots, unsigned long long *__restrict__ out)
+{
+    const int32_t *row = counts + (int64_t)blockIdx.x * stride;
+    unsigned long long s = 0;
+    for (int64_t t = threadIdx.x; t < slots; t += 256) s += (unsigned long long)row[t];
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
+    __shared__ unsigned long long s_w[4];
+    if ((threadIdx.x & 63) == 0) s_w[threadIdx.x >> 6] = s;
+    __syncthreads();
+    if (threadIdx.x == 0) out[blockIdx.x] = s_w[0] + s_w[1] + s_w[2] + s_w[3];
+}
+
+hipError_t launch_reduce_counts(const int32_t *counts, int64_t stride, int64_t slots, int32_t rows,
+                                unsigned long long *out, hipStream_t s)
+{
+    if (rows <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_reduce_counts, dim3((unsigned)rows), dim3(256), 0, s, counts, stride, slots, out);
+    return hipGetLastError();
+}
+
+int64_t count_slots(int kernel, int64_t n, int64_t n_waves)
+{
+    return kernel == 1 ? ((n + 255) / 256) * 4 : n_waves;
 }
 
 // ---------------------------------------------------------------------------

@@ -290,12 +290,31 @@ __global__ void k_partition(const int64_t *__restrict__ row_ptr, int64_t n, int3
     part[w] = (int32_t)lo;
 }
 
-hipError_t launch_partition(const int64_t *row_ptr, int64_t n, int32_t dim, int32_t *part, int64_t n_waves,
-                            hipStream_t s)
+// head[e] = row of edge e minus the first row of its wave (< rows_cap <= 256).
+// One thread per row: its wave is the last w with part[w] <= row.
+__global__ void k_head_local(const int64_t *__restrict__ row_ptr, int64_t n, const int32_t *__restrict__ part,
+                             int64_t n_waves, uint8_t *__restrict__ head)
 {
+    const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (r >= n) return;
+    int64_t lo = 0, hi = n_waves - 1;
+    while (lo < hi) {
+        int64_t mid = (lo + hi + 1) >> 1;
+        if (part[mid] <= r) lo = mid; else hi = mid - 1;
+    }
+    const uint8_t h = (uint8_t)(r - part[lo]);
+    for (int64_t e = row_ptr[r]; e < row_ptr[r + 1]; ++e) head[e] = h;
+}
+
+hipError_t launch_partition(const int64_t *row_ptr, int64_t n, int32_t dim, int32_t *part, int64_t n_waves,
+                            uint8_t *head, hipStream_t s)
+{
+    static_assert(rows_cap(1) <= 256 && rows_cap(16) <= 256, "head offsets must fit in a byte");
     int64_t blocks = (n_waves + 1 + 255) / 256;
     hipLaunchKernelGGL(k_partition, dim3((unsigned)blocks), dim3(256), 0, s, row_ptr, n, row_weight(dim), part,
                        n_waves);
+    hipLaunchKernelGGL(k_head_local, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, row_ptr, n, part, n_waves,
+                       head);
     return hipGetLastError();
 }
 

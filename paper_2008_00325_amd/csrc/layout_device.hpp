@@ -30,22 +30,20 @@ struct Ctr {
 };
 
 // Philox4x32 with 10 rounds.  Each round multiplies counter words 0 and 2 by
-// the two round constants; the high halves are mixed with words 1 and 3 and
-// the round key, and the key advances by the two Weyl increments.
+// the two round constants (full 64-bit products, one v_mad_u64_u32 each); the
+// high halves are mixed with words 1 and 3 and the round key, and the key
+// advances by the two Weyl increments.
 __device__ __forceinline__ Ctr philox4x32_10(Ctr c, uint32_t key_lo, uint32_t key_hi)
 {
 #pragma unroll
     for (int round = 0; round < 10; ++round) {
-        const uint32_t m0 = 0xD2511F53u, m1 = 0xCD9E8D57u;
-        uint32_t hi0 = __umulhi(m0, c.w[0]);
-        uint32_t lo0 = m0 * c.w[0];
-        uint32_t hi1 = __umulhi(m1, c.w[2]);
-        uint32_t lo1 = m1 * c.w[2];
+        const uint64_t p0 = (uint64_t)0xD2511F53u * c.w[0];
+        const uint64_t p1 = (uint64_t)0xCD9E8D57u * c.w[2];
         Ctr nx;
-        nx.w[0] = hi1 ^ c.w[1] ^ key_lo;
-        nx.w[1] = lo1;
-        nx.w[2] = hi0 ^ c.w[3] ^ key_hi;
-        nx.w[3] = lo0;
+        nx.w[0] = (uint32_t)(p1 >> 32) ^ c.w[1] ^ key_lo;
+        nx.w[1] = (uint32_t)p1;
+        nx.w[2] = (uint32_t)(p0 >> 32) ^ c.w[3] ^ key_hi;
+        nx.w[3] = (uint32_t)p0;
         c = nx;
         key_lo += 0x9E3779B9u;
         key_hi += 0xBB67AE85u;
@@ -80,20 +78,26 @@ __device__ __forceinline__ bool edge_active(float eps, int32_t epoch)
 
 __device__ __forceinline__ float clip4(float g) { return fminf(fmaxf(g, -kClip), kClip); }
 
-// Attraction: d/dy_i log Phi = c (y_i - y_j), c = -2ab d2^(b-1) / (1 + a d2^b).
+// d2^b for d2 > 0 by the hardware base-2 logarithm and exponential.
+__device__ __forceinline__ float pow_b(float d2, float b) { return __builtin_amdgcn_exp2f(b * __builtin_amdgcn_logf(d2)); }
+
+// Attraction: d/dy_i log Phi = c (y_i - y_j), c = -2ab d2^(b-1) / (1 + a d2^b),
+// written as -2ab d2^b / (d2 (1 + a d2^b)) with one hardware reciprocal; 0
+// when the points coincide.  Branch-free (the guard is a select).
 __device__ __forceinline__ float attraction_coef(float d2, float a, float b)
 {
-    if (!(d2 > 0.0f)) return 0.0f;
-    float p = exp2f(b * log2f(d2));   // d2^b
-    return -2.0f * a * b * p / (d2 * (1.0f + a * p));
+    const float p = pow_b(d2, b);
+    const float c = (-2.0f * a * b * p) * __builtin_amdgcn_rcpf(d2 * fmaf(a, p, 1.0f));
+    return d2 > 0.0f ? c : 0.0f;
 }
 
-// Repulsion: d/dy_i log(1 - Phi) = c (y_i - y_k), c = 2b / ((1e-3 + d2)(1 + a d2^b)).
+// Repulsion: d/dy_i log(1 - Phi) = c (y_i - y_k), c = 2b / ((1e-3 + d2)(1 + a d2^b));
+// 0 when the points coincide.  Branch-free.
 __device__ __forceinline__ float repulsion_coef(float d2, float a, float b)
 {
-    if (!(d2 > 0.0f)) return 0.0f;
-    float p = exp2f(b * log2f(d2));
-    return 2.0f * b / ((kRepEps + d2) * (1.0f + a * p));
+    const float p = pow_b(d2, b);
+    const float c = (2.0f * b) * __builtin_amdgcn_rcpf((kRepEps + d2) * fmaf(a, p, 1.0f));
+    return d2 > 0.0f ? c : 0.0f;
 }
 
 struct EpochArgs {
@@ -105,53 +109,79 @@ struct EpochArgs {
     float a, b;
     double alpha;        // 1 - epoch / n_epochs
     uint32_t key_lo, key_hi;
-    unsigned long long *active_count;  // += sampled edges of this epoch
+    int32_t *counts;     // this epoch's row of per-wave sampled-edge counts
 };
 
-// Everything one sampled edge e = (i -> j) contributes to vertex i, in
-// fixed point: twice the clipped attraction (its own "move the source" share
-// plus the equal share of the reverse edge (j -> i), which is sampled in the
-// same epochs because B is symmetric with bit-equal weights), then the clipped
-// repulsions of its negative samples (a draw equal to i is skipped).  The step
-// size is applied once per vertex at the end of the epoch.
 template <int DIM>
-__device__ __forceinline__ void edge_contribution(const EpochArgs &A, int64_t e, uint32_t i, uint32_t j,
-                                                  const float (&yi)[DIM], long long (&fx)[DIM])
+__device__ __forceinline__ float sq_dist(const float (&x)[DIM], const float (&y)[DIM], float (&diff)[DIM])
 {
-    const float *__restrict__ E = A.E;
-    float diff[DIM];
     float d2 = 0.0f;
 #pragma unroll
     for (int d = 0; d < DIM; ++d) {
-        diff[d] = yi[d] - E[(size_t)j * DIM + d];
-        d2 += diff[d] * diff[d];
+        diff[d] = x[d] - y[d];
+        d2 = fmaf(diff[d], diff[d], d2);
     }
-    double s[DIM];
-    float c = attraction_coef(d2, A.a, A.b);
-#pragma unroll
-    for (int d = 0; d < DIM; ++d) s[d] = 2.0 * (double)clip4(c * diff[d]);
+    return d2;
+}
 
-    for (int32_t q = 0; q * 4 < A.neg_rate; ++q) {
-        Ctr w = negative_words(e, A.epoch, q, A.key_lo, A.key_hi);
+template <int DIM>
+__device__ __forceinline__ void load_row(const float *__restrict__ E, uint32_t v, float (&y)[DIM])
+{
 #pragma unroll
-        for (int32_t t = 0; t < 4; ++t) {
-            if (4 * q + t >= A.neg_rate) break;
-            uint32_t k = word_to_vertex(w.w[t], A.n);
-            if (k == i) continue;
-            float dk[DIM];
-            float q2 = 0.0f;
+    for (int d = 0; d < DIM; ++d) y[d] = E[(size_t)v * DIM + d];
+}
+
+// One update term in fixed point: round(t * 2^32) to nearest (ties to even),
+// by adding the 1.5 * 2^52 shifter in fp64 (exact for |t| < 2^19) and
+// reading the integer out of the mantissa.  Every term is converted on its
+// own, so the integer sum of a vertex's terms does not depend on how the
+// terms are grouped into kernels, lanes or waves.
+__device__ __forceinline__ long long to_fixed(float t)
+{
+    const double shifter = 0x1.8p52;
+    const double y = fma((double)t, kFixOne, shifter);
+    return (long long)(__double_as_longlong(y) - __double_as_longlong(shifter));
+}
+
+// Attraction share of vertex i for a sampled edge (i -> j): twice the clipped
+// gradient of log Phi -- its own "move the source" share plus the equal share
+// of the reverse edge (j -> i), which is sampled in the same epochs because B
+// is symmetric with bit-equal weights.
+template <int DIM>
+__device__ __forceinline__ void attraction_fixed(const float (&yi)[DIM], const float (&yj)[DIM], float a, float b,
+                                                 long long (&fx)[DIM])
+{
+    float diff[DIM];
+    const float d2 = sq_dist<DIM>(yi, yj, diff);
+    const float c = attraction_coef(d2, a, b);
 #pragma unroll
-            for (int d = 0; d < DIM; ++d) {
-                dk[d] = yi[d] - E[(size_t)k * DIM + d];
-                q2 += dk[d] * dk[d];
-            }
-            float cr = repulsion_coef(q2, A.a, A.b);
+    for (int d = 0; d < DIM; ++d) fx[d] = to_fixed(2.0f * clip4(c * diff[d]));
+}
+
+// Repulsion of vertex i from a negative sample k (callers skip k == i).
+template <int DIM>
+__device__ __forceinline__ void repulsion_fixed(const float (&yi)[DIM], const float (&yk)[DIM], float a, float b,
+                                                long long (&fx)[DIM])
+{
+    float diff[DIM];
+    const float d2 = sq_dist<DIM>(yi, yk, diff);
+    const float c = repulsion_coef(d2, a, b);
 #pragma unroll
-            for (int d = 0; d < DIM; ++d) s[d] += (double)clip4(cr * dk[d]);
-        }
+    for (int d = 0; d < DIM; ++d) fx[d] = to_fixed(clip4(c * diff[d]));
+}
+
+// The random words of negative samples 0 .. 4*NQ-1 of edge e; NQ > 0 draws
+// them all at once (neg_rate <= 4 NQ).
+template <int NQ>
+__device__ __forceinline__ void negative_words_all(int64_t e, int32_t epoch, uint32_t key_lo, uint32_t key_hi,
+                                                   uint32_t (&u)[4 * NQ])
+{
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+        Ctr w = negative_words(e, epoch, q, key_lo, key_hi);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) u[4 * q + t] = w.w[t];
     }
-#pragma unroll
-    for (int d = 0; d < DIM; ++d) fx[d] = __double2ll_rn(s[d] * kFixOne);
 }
 
 // E_{n+1}[i][d] = E_n[i][d] + alpha * (accumulated fixed-point sum).
