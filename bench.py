@@ -23,6 +23,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -33,8 +34,11 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
-PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "epoch_traffic_window1m.json")
-KERNEL_SOURCES = ["paper_2008_00325_amd/csrc/kernels_layout.hip", "paper_2008_00325_amd/csrc/layout_device.hpp"]
+# HBM traffic of one epoch from rocprofv3 FETCH_SIZE / WRITE_SIZE passes (scaled by the
+# same counters on the library's copy probe); valid while the kernel sources hash the same
+PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "epoch_window1m.md")
+KERNEL_SOURCES = ["paper_2008_00325_amd/csrc/kernels_layout.hip", "paper_2008_00325_amd/csrc/layout_device.hpp",
+                  "paper_2008_00325_amd/csrc/internal.hpp"]
 
 
 def log(msg: str) -> None:
@@ -47,6 +51,22 @@ def kernel_hash() -> str:
         with open(os.path.join(ROOT, p), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
+
+
+def profiled_traffic(workload: str):
+    """Bytes per epoch recorded in the profile summary, if it was taken on the
+    current kernel sources and this workload; else None."""
+    if not os.path.exists(PROFILE_TRAFFIC):
+        return None
+    fields = {}
+    with open(PROFILE_TRAFFIC) as f:
+        for line in f:
+            m = re.match(r"^- (kernel_hash|workload|traffic_bytes_per_epoch): `?([^`\s]+)`?", line.strip())
+            if m:
+                fields[m.group(1)] = m.group(2)
+    if fields.get("kernel_hash") != kernel_hash() or fields.get("workload") != workload:
+        return None
+    return float(fields["traffic_bytes_per_epoch"])
 
 
 def algorithmic_bytes_per_epoch(n: int, dim: int, nnz: int, active: float, neg_rate: int) -> float:
@@ -122,7 +142,7 @@ def copy_probe(torch, U, mb: int = 1024, reps: int = 5) -> float:
     return 2.0 * nbytes / (ms * 1e-3) / 1e9
 
 
-def cpu_baseline(w, ids, dist, budget_s: float = 20.0):
+def cpu_baseline(w, ids, dist, budget_s: float = 12.0):
     """The C oracle (fp64 push-form Jacobi epochs) timed on the host cores, on
     a sample of epochs spread over the run, from the random initial layout."""
     import oracle as O
@@ -133,7 +153,15 @@ def cpu_baseline(w, ids, dist, budget_s: float = 20.0):
     a, b = O.fit_ab(w.spread, w.min_dist)
     E = O.init_layout(w.n, w.dim, 0).astype(np.float64)
     log(f"oracle graph ready in {time.time() - t0:.1f}s ({g.nnz} edges); timing epochs")
-    sample = [0, 100, 199, 50, 150, 25, 75, 125, 175]
+    # epochs spread over the run (bisection order) until about budget_s of CPU time
+    sample, seen = [], set()
+    step = w.n_epochs
+    while step >= 1 and len(sample) < w.n_epochs:
+        for ep in range(0, w.n_epochs, step):
+            if ep not in seen:
+                seen.add(ep)
+                sample.append(ep)
+        step //= 2
     done, updates, spent = [], 0, 0.0
     for ep in sample:
         t1 = time.perf_counter()
@@ -148,8 +176,9 @@ def cpu_baseline(w, ids, dist, budget_s: float = 20.0):
         "unit": "edge-updates/s",
         "cores": O.num_threads(),
         "kind": "oracle",
-        "sample": f"epochs {done} of the {w.n_epochs}-epoch {w.name} layout from the random initial layout "
-                  f"(fp64 push form, {updates} edge updates in {spent:.2f} s)",
+        "sample": f"{len(done)} of the {w.n_epochs} epochs of the {w.name} layout (spread over the run: "
+                  f"{done[:6]}...), each from the random initial layout; fp64 push form, "
+                  f"{updates} edge updates in {spent:.2f} s",
     }
 
 
@@ -192,12 +221,7 @@ def main() -> int:
     bytes_epoch = algorithmic_bytes_per_epoch(w.n, w.dim, st["nnz_kept"], avg_active, w.neg_rate)
     launch_ms = epochs_ms / n_epochs
     achieved = bytes_epoch / (launch_ms * 1e-3) / 1e9
-    traffic = None
-    if os.path.exists(PROFILE_TRAFFIC):
-        with open(PROFILE_TRAFFIC) as f:
-            prof = json.load(f)
-        if prof.get("kernel_hash") == kernel_hash() and prof.get("workload") == w.name:
-            traffic = prof.get("bytes_per_launch")
+    traffic = profiled_traffic(w.name)
     copy_gbps = copy_probe(torch, U)
     gpu_name = torch.cuda.get_device_name(0)
 
@@ -227,7 +251,7 @@ def main() -> int:
         "edge_updates_per_step": st["edge_updates"],
         "roofline": {
             "bound": "hbm",
-            "kernel": "k_epoch_wave<2>",
+            "kernel": f"epoch = k_epoch_draw + {st['table_ranges']} x k_epoch_repulse",
             "achieved": achieved,
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",

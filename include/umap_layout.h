@@ -64,6 +64,9 @@ typedef struct {
     double prep_ms;         /* device time of the ingest inside create           */
     double init_ms;         /* device time of the random initialisation (run)    */
     double epochs_ms;       /* device time of the last call's epoch launches     */
+    int32_t table_ranges;   /* P: an epoch is one draw launch and P repulsion
+                               launches, each gathering from 1/P of the table   */
+    int32_t kernel;         /* epoch kernel in use (see umap_layout_set_kernel)  */
 } umap_layout_stats_t;
 
 /*

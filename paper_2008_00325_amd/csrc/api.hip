@@ -512,6 +512,8 @@ int umap_layout_stats(const umap_layout *h, umap_layout_stats_t *out)
     s.nnz_kept = h->nnz;
     s.max_degree = h->max_degree;
     s.w_max = h->w_max;
+    s.table_ranges = 1 << h->lg_phases;
+    s.kernel = h->kernel;
     *out = s;
     return UMAP_OK;
 }

@@ -50,6 +50,8 @@ class umap_layout_stats_t(ctypes.Structure):
         ("prep_ms", ctypes.c_double),
         ("init_ms", ctypes.c_double),
         ("epochs_ms", ctypes.c_double),
+        ("table_ranges", ctypes.c_int32),
+        ("kernel", ctypes.c_int32),
     ]
 
     def as_dict(self) -> dict:
