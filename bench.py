@@ -46,10 +46,15 @@ def log(msg: str) -> None:
 
 
 def kernel_hash() -> str:
+    """Hash of the epoch kernels' code with comments and whitespace removed, so
+    that an edit of the comments keeps the recorded profile valid."""
     h = hashlib.sha256()
     for p in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, p), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, p)) as f:
+            text = f.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 

@@ -1,20 +1,16 @@
 // kernels_layout.hip -- random initialisation and the epoch kernels of the
 // layout SGD (UMAP section objective; embedding-updates section), gfx950.
 //
-// Both epoch kernels implement one epoch-synchronous step: every read sees the
-// snapshot E_n, every vertex's updates are summed in a fixed-point int64
-// accumulator, and E_{n+1} = E_n + alpha * sum is written to the other buffer
-// (no scatter to global memory, no global atomics on the embedding).
-//  * k_epoch_wave:    edge-parallel.  Each wavefront owns a range of whole rows
-//                     (balanced by edges + rows).  It streams the rows' eps,
-//                     compacts the sampled edges into its slice of a scratch
-//                     list, then runs full 64-lane batches in which each lane
-//                     handles one sampled edge: its attraction and its
-//                     negative samples.  Sums go to a per-wave LDS accumulator
-//                     with 64-bit integer atomics; the wave then writes its
-//                     rows of E_{n+1} with coalesced stores.
+// Both epoch paths implement one epoch-synchronous step: every read sees the
+// snapshot E_n, every term is converted to fixed point on its own and summed in
+// int64, and E_{n+1} = E_n + alpha * sum is written to the other buffer (no
+// scatter to global memory, no atomics on the embedding in global memory).
+//  * edge-parallel (default): one k_epoch_draw launch and P k_epoch_repulse
+//    launches per epoch, each wavefront owning a range of whole rows (see the
+//    section comment below).
 //  * k_epoch_rowwise: one thread per vertex walking its row (a plain second
-//                     implementation used to cross-check the first).
+//    implementation used to cross-check the first).
+// Because the sums are exact integers, both paths give the same bits.
 #include "internal.hpp"
 
 namespace ul {
