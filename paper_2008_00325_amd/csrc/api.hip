@@ -125,9 +125,6 @@ struct umap_layout {
     int32_t *part = nullptr;
     int64_t n_waves = 0;
     uint8_t *head = nullptr;       // edge's row relative to its wave's first row
-    int32_t *act_edge = nullptr;   // per-epoch scratch list of sampled edges
-    int32_t *act_tail = nullptr;
-    uint8_t *act_head = nullptr;
     float *E[2] = {nullptr, nullptr};
     int cur = 0;
     bool has_layout = false;
@@ -187,8 +184,8 @@ int create_common(umap_layout **out, int64_t n, int32_t dim, const int32_t *rows
         const int32_t lg_phases = ul::phase_log2(n, dim);
         const int64_t n_phases = (int64_t)1 << lg_phases;
         size_t bytes = need<int64_t>(n + 1) + need<int32_t>(nnz) + need<float>(nnz) + need<int32_t>(max_waves + 1) +
-                       2 * need<float>(nd) + need<unsigned long long>(n_epochs) + 2 * need<uint8_t>(nnz) +
-                       2 * need<int32_t>(nnz) + need<int32_t>((size_t)count_rows * count_stride) +
+                       2 * need<float>(nd) + need<unsigned long long>(n_epochs) + need<uint8_t>(nnz) +
+                       need<int32_t>((size_t)count_rows * count_stride) +
                        need<uint32_t>((size_t)n_phases * neg_rate * nnz) + need<int32_t>((size_t)n_phases * max_waves) +
                        need<long long>(nd);
         if (fault_alloc()) throw HipFailure{hipErrorOutOfMemory, "hipMalloc(arena) [injected]"};
@@ -202,9 +199,6 @@ int create_common(umap_layout **out, int64_t n, int32_t dim, const int32_t *rows
         h->E[1] = cv.take<float>(nd);
         h->active = cv.take<unsigned long long>(n_epochs);
         h->head = cv.take<uint8_t>(nnz);
-        h->act_edge = cv.take<int32_t>(nnz);
-        h->act_tail = cv.take<int32_t>(nnz);
-        h->act_head = cv.take<uint8_t>(nnz);
         h->counts = cv.take<int32_t>((size_t)count_rows * count_stride);
         h->count_stride = count_stride;
         h->lg_phases = lg_phases;
@@ -315,13 +309,17 @@ int run_epochs_impl(umap_layout *h, uint64_t seed, int32_t first, int32_t last, 
     A.key_lo = (uint32_t)seed;
     A.key_hi = (uint32_t)(seed >> 32);
     ul::WaveGraph G{h->row_ptr, h->col,      h->eps,      h->head,     h->part,
-                    h->n_waves,  h->act_edge, h->act_tail, h->act_head, 1 << h->lg_phases,
+                    h->n_waves,  1 << h->lg_phases,
                     h->lg_phases, h->rec,     (int64_t)h->neg_rate * h->nnz, h->rec_count, h->delta};
     UL_HIP(ul::launch_zero_u64(h->active, h->n_epochs, h->stream));
     UL_HIP(hipEventRecord(h->ev[1], h->stream));
-    // the wave kernels store a sample's offset inside its table range in 24
-    // bits; beyond that (n >= 2^28 vertices) the one-thread-per-vertex kernel runs
-    const int kernel = ((h->n >> h->lg_phases) + 2 < ((int64_t)1 << 24)) ? h->kernel : 1;
+    // the wave kernels store a sample's offset inside its table range and a
+    // sampled edge's offset inside its wave in 24 bits (a wave holds fewer
+    // than kWaveCost + max_degree edges); beyond that (n >= 2^28 vertices, or
+    // a row of about 2^24 edges) the one-thread-per-vertex kernel runs
+    const bool fits = (h->n >> h->lg_phases) + 2 < ((int64_t)1 << 24) &&
+                      (int64_t)h->max_degree + ul::kWaveCost < ((int64_t)1 << 24);
+    const int kernel = fits ? h->kernel : 1;
     const int64_t slots = ul::count_slots(kernel, h->n, h->n_waves);
     const int ring = h->n_epochs < ul::kCountRing ? h->n_epochs : ul::kCountRing;
     int32_t pending_from = first;   // first epoch whose counts are not yet summed

@@ -77,9 +77,6 @@ struct WaveGraph {
     const uint8_t *head;      // row of each edge relative to its wave's first row
     const int32_t *part;      // n_waves + 1 wave boundaries (rows)
     int64_t n_waves;
-    int32_t *act_edge;        // scratch: sampled edges of the epoch, per wave slice
-    int32_t *act_tail;
-    uint8_t *act_head;
     // negative samples are filed by vertex-table range: P = 2^lg_phases ranges
     int32_t n_phases;
     int32_t lg_phases;

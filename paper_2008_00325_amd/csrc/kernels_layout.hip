@@ -121,7 +121,12 @@ constexpr int kWavesPerBlock = 4;
 // classified.
 constexpr int kSuper = 4;
 // Records per lane per step of the repulsion kernel.
-constexpr int kRepUnroll = 8;
+constexpr int kRepUnroll = 16;
+// LDS ring of sampled edges waiting for their attraction and draws
+// ((row in wave) << 24 | edge offset in wave): holds the < 64 left over plus
+// one super-chunk.
+constexpr int kQueue = 512;
+static_assert(kQueue >= kWave - 1 + kSuper * kWave, "queue too small");
 
 __device__ __forceinline__ int64_t uniform64(int64_t v)
 {
@@ -154,6 +159,7 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
     __shared__ long long s_acc[kWavesPerBlock][CAP * DIM];
     __shared__ float s_y[kWavesPerBlock][CAP * DIM];   // the wave's own rows of E_n
     __shared__ uint32_t s_rec[kWavesPerBlock][kMaxPhases];
+    __shared__ uint32_t s_q[kWavesPerBlock][kQueue];
 
     const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const unsigned lane = threadIdx.x % kWave;
@@ -183,56 +189,20 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
     int64_t qn = 0;
     // loads are unconditional (the index is clamped into the wave's range and
     // the value masked) so that the next super-chunk stays in flight
-    auto load_super = [&](int64_t sbase, float (&ev)[kSuper], int32_t (&cv)[kSuper], uint8_t (&hv)[kSuper]) {
+    auto load_super = [&](int64_t sbase, float (&ev)[kSuper], uint8_t (&hv)[kSuper]) {
 #pragma unroll
         for (int j = 0; j < kSuper; ++j) {
             int64_t e = sbase + j * kWave + lane;
             e = e < e1 ? e : e1 - 1;
             ev[j] = G.eps[e];
-            cv[j] = G.col[e];
             hv[j] = G.head[e];
         }
     };
-    auto scan_super = [&](int64_t sbase, const float (&ev)[kSuper], const int32_t (&cv)[kSuper],
-                          const uint8_t (&hv)[kSuper]) {
-#pragma unroll
-        for (int j = 0; j < kSuper; ++j) {
-            const int64_t e = sbase + j * kWave + lane;
-            if (sbase + j * kWave >= e1) break;
-            const bool act = edge_active(ev[j], A.epoch) & (e < e1);
-            const unsigned long long m = __ballot(act);
-            if (act) {
-                const int64_t pos = e0 + qn + lanes_below(m);
-                G.act_edge[pos] = (int32_t)e;
-                G.act_tail[pos] = cv[j];
-                G.act_head[pos] = hv[j];
-            }
-            qn += __popcll(m);
-        }
-    };
-    if (e1 > e0) {
-        float ea[kSuper], eb[kSuper];
-        int32_t ca[kSuper], cb[kSuper];
-        uint8_t ha[kSuper], hb[kSuper];
-        constexpr int64_t kStep = (int64_t)kSuper * kWave;
-        load_super(e0, ea, ca, ha);
-        for (int64_t s0 = e0; s0 < e1; s0 += 2 * kStep) {
-            load_super(s0 + kStep, eb, cb, hb);
-            scan_super(s0, ea, ca, ha);
-            if (s0 + kStep >= e1) break;
-            load_super(s0 + 2 * kStep, ea, ca, ha);
-            scan_super(s0 + kStep, eb, cb, hb);
-        }
-    }
-    // the list written by this wave's lanes is read back by other lanes of
-    // the same wave (same CU)
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
-
-    // ---- attraction + negative draws, 64 sampled edges per batch ------------
     const int32_t R = A.neg_rate;
     const int32_t lg = G.lg_phases;
     uint32_t *const rec_wave = G.rec + (int64_t)R * e0;   // this wave's slice of every range
+    uint32_t *q = s_q[wv];
+    uint32_t qhead = 0, qtail = 0;
     auto file = [&](uint32_t u, uint32_t i, int h) {
         const uint32_t k = word_to_vertex(u, A.n);
         if (k == i) return;   // a draw equal to the source adds nothing
@@ -240,12 +210,13 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
         const uint32_t slot = atomicAdd(&rec_n[p], 1u);
         rec_wave[(int64_t)p * G.rec_stride + slot] = ((uint32_t)h << 24) | (k - range_base(p, lg, A.n));
     };
-    for (int64_t b = 0; b < qn; b += kWave) {
-        const bool valid = b + lane < qn;
-        const int64_t slot = valid ? e0 + b + lane : e0;
-        const int64_t e = G.act_edge[slot];
-        const uint32_t tail = (uint32_t)G.act_tail[slot];
-        const int h = G.act_head[slot];
+    // attraction and negative draws of `count` queued sampled edges
+    auto process = [&](int count) {
+        const bool valid = (int)lane < count;
+        const uint32_t ent = q[(qhead + lane) & (kQueue - 1)];
+        const int h = valid ? (int)(ent >> 24) : 0;
+        const int64_t e = valid ? e0 + (ent & 0xFFFFFFu) : e0;
+        const uint32_t tail = (uint32_t)G.col[e];
         const uint32_t i = (uint32_t)(r0 + h);
         float yi[DIM], yj[DIM];
 #pragma unroll
@@ -264,14 +235,51 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
                 for (int r = 0; r < 4 * NQ; ++r)
                     if (r < R) file(u[r], i, h);
             } else {
-                for (int32_t q = 0; 4 * q < R; ++q) {
-                    Ctr wd = negative_words(e, A.epoch, q, A.key_lo, A.key_hi);
+                for (int32_t qq = 0; 4 * qq < R; ++qq) {
+                    Ctr wd = negative_words(e, A.epoch, qq, A.key_lo, A.key_hi);
 #pragma unroll
                     for (int t = 0; t < 4; ++t)
-                        if (4 * q + t < R) file(wd.w[t], i, h);
+                        if (4 * qq + t < R) file(wd.w[t], i, h);
                 }
             }
         }
+        qhead += (uint32_t)count;
+    };
+    auto scan_super = [&](int64_t sbase, const float (&ev)[kSuper], const uint8_t (&hv)[kSuper]) {
+#pragma unroll
+        for (int j = 0; j < kSuper; ++j) {
+            const int64_t e = sbase + j * kWave + lane;
+            if (sbase + j * kWave >= e1) break;
+            const bool act = edge_active(ev[j], A.epoch) & (e < e1);
+            const unsigned long long m = __ballot(act);
+            if (act) q[(qtail + lanes_below(m)) & (kQueue - 1)] = ((uint32_t)hv[j] << 24) | (uint32_t)(e - e0);
+            const uint32_t nact = (uint32_t)__popcll(m);
+            qn += nact;
+            qtail += nact;
+        }
+        if (qtail - qhead >= (uint32_t)kWave) {
+            wave_sync();
+            do {
+                process(kWave);
+            } while (qtail - qhead >= (uint32_t)kWave);
+        }
+    };
+    if (e1 > e0) {
+        float ea[kSuper], eb[kSuper];
+        uint8_t ha[kSuper], hb[kSuper];
+        constexpr int64_t kStep = (int64_t)kSuper * kWave;
+        load_super(e0, ea, ha);
+        for (int64_t s0 = e0; s0 < e1; s0 += 2 * kStep) {
+            load_super(s0 + kStep, eb, hb);
+            scan_super(s0, ea, ha);
+            if (s0 + kStep >= e1) break;
+            load_super(s0 + 2 * kStep, ea, ha);
+            scan_super(s0 + kStep, eb, hb);
+        }
+    }
+    if (qtail != qhead) {
+        wave_sync();
+        process((int)(qtail - qhead));
     }
     wave_sync();
 
