@@ -119,13 +119,17 @@ constexpr int kWavesPerBlock = 4;
 // The eps / col / head stream is read in super-chunks of kSuper x 64 edges,
 // double buffered in registers: super-chunk s+1 is in flight while s is
 // classified.
-constexpr int kSuper = 4;
+constexpr int kSuper = 2;
+// Rows staged in LDS on each side of a wave's own rows: the attraction reads
+// y_j from there when j is that close (neighbour lists of locally ordered
+// vertices), and from global memory otherwise.
+constexpr int kHalo = 64;
 // Records per lane per step of the repulsion kernel.
 constexpr int kRepUnroll = 16;
-// LDS ring of sampled edges waiting for their attraction and draws
-// ((row in wave) << 24 | edge offset in wave): holds the < 64 left over plus
+// LDS ring of sampled edges waiting for their attraction and draws: (tail,
+// (row in wave) << 24 | edge offset in wave); holds the < 64 left over plus
 // one super-chunk.
-constexpr int kQueue = 512;
+constexpr int kQueue = 256;
 static_assert(kQueue >= kWave - 1 + kSuper * kWave, "queue too small");
 
 __device__ __forceinline__ int64_t uniform64(int64_t v)
@@ -157,9 +161,9 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
 {
     constexpr int CAP = rows_cap(DIM);
     __shared__ long long s_acc[kWavesPerBlock][CAP * DIM];
-    __shared__ float s_y[kWavesPerBlock][CAP * DIM];   // the wave's own rows of E_n
+    __shared__ float s_y[kWavesPerBlock][(CAP + 2 * kHalo) * DIM];   // the wave's rows of E_n and halos
     __shared__ uint32_t s_rec[kWavesPerBlock][kMaxPhases];
-    __shared__ uint32_t s_q[kWavesPerBlock][kQueue];
+    __shared__ uint2 s_q[kWavesPerBlock][kQueue];
 
     const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const unsigned lane = threadIdx.x % kWave;
@@ -176,32 +180,34 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
     const int64_t e1 = uniform64(G.row_ptr[r0 + nrows]);
 
     long long *acc = s_acc[wv];
-    float *yrows = s_y[wv];
+    float *yrows = s_y[wv] + kHalo * DIM;   // row h of the wave at yrows[h * DIM], h in [-kHalo, nrows + kHalo)
     uint32_t *rec_n = s_rec[wv];
     const size_t g0 = (size_t)r0 * DIM;
-    for (int t = lane; t < nrows * DIM; t += kWave) {
-        acc[t] = 0;
-        yrows[t] = A.E[g0 + t];
-    }
+    // staged rows [lo, hi): the wave's own rows and up to kHalo on each side
+    const int64_t lo = r0 >= kHalo ? r0 - kHalo : 0;
+    const int64_t hi = r0 + nrows + kHalo <= (int64_t)A.n ? r0 + nrows + kHalo : (int64_t)A.n;
+    for (int t = lane; t < nrows * DIM; t += kWave) acc[t] = 0;
+    for (int64_t t = (lo - r0) * DIM + lane; t < (hi - r0) * DIM; t += kWave) yrows[t] = A.E[(int64_t)g0 + t];
     if ((int)lane < kMaxPhases) rec_n[lane] = 0;
 
     // ---- classify and compact ----------------------------------------------
     int64_t qn = 0;
     // loads are unconditional (the index is clamped into the wave's range and
     // the value masked) so that the next super-chunk stays in flight
-    auto load_super = [&](int64_t sbase, float (&ev)[kSuper], uint8_t (&hv)[kSuper]) {
+    auto load_super = [&](int64_t sbase, float (&ev)[kSuper], int32_t (&cv)[kSuper], uint8_t (&hv)[kSuper]) {
 #pragma unroll
         for (int j = 0; j < kSuper; ++j) {
             int64_t e = sbase + j * kWave + lane;
             e = e < e1 ? e : e1 - 1;
             ev[j] = G.eps[e];
+            cv[j] = G.col[e];
             hv[j] = G.head[e];
         }
     };
     const int32_t R = A.neg_rate;
     const int32_t lg = G.lg_phases;
     uint32_t *const rec_wave = G.rec + (int64_t)R * e0;   // this wave's slice of every range
-    uint32_t *q = s_q[wv];
+    uint2 *q = s_q[wv];
     uint32_t qhead = 0, qtail = 0;
     auto file = [&](uint32_t u, uint32_t i, int h) {
         const uint32_t k = word_to_vertex(u, A.n);
@@ -213,15 +219,20 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
     // attraction and negative draws of `count` queued sampled edges
     auto process = [&](int count) {
         const bool valid = (int)lane < count;
-        const uint32_t ent = q[(qhead + lane) & (kQueue - 1)];
-        const int h = valid ? (int)(ent >> 24) : 0;
-        const int64_t e = valid ? e0 + (ent & 0xFFFFFFu) : e0;
-        const uint32_t tail = (uint32_t)G.col[e];
+        const uint2 ent = q[(qhead + lane) & (kQueue - 1)];
+        const int h = valid ? (int)(ent.y >> 24) : 0;
+        const int64_t e = valid ? e0 + (ent.y & 0xFFFFFFu) : e0;
+        const uint32_t tail = valid ? ent.x : (uint32_t)r0;
         const uint32_t i = (uint32_t)(r0 + h);
         float yi[DIM], yj[DIM];
 #pragma unroll
         for (int d = 0; d < DIM; ++d) yi[d] = yrows[h * DIM + d];
-        load_row<DIM>(A.E, tail, yj);
+        if ((int64_t)tail >= lo && (int64_t)tail < hi) {
+#pragma unroll
+            for (int d = 0; d < DIM; ++d) yj[d] = yrows[((int64_t)tail - r0) * DIM + d];
+        } else {
+            load_row<DIM>(A.E, tail, yj);
+        }
         long long fx[DIM];
         attraction_fixed<DIM>(yi, yj, A.a, A.b, fx);
         if (valid) {
@@ -245,14 +256,17 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
         }
         qhead += (uint32_t)count;
     };
-    auto scan_super = [&](int64_t sbase, const float (&ev)[kSuper], const uint8_t (&hv)[kSuper]) {
+    auto scan_super = [&](int64_t sbase, const float (&ev)[kSuper], const int32_t (&cv)[kSuper],
+                          const uint8_t (&hv)[kSuper]) {
 #pragma unroll
         for (int j = 0; j < kSuper; ++j) {
             const int64_t e = sbase + j * kWave + lane;
             if (sbase + j * kWave >= e1) break;
             const bool act = edge_active(ev[j], A.epoch) & (e < e1);
             const unsigned long long m = __ballot(act);
-            if (act) q[(qtail + lanes_below(m)) & (kQueue - 1)] = ((uint32_t)hv[j] << 24) | (uint32_t)(e - e0);
+            if (act)
+                q[(qtail + lanes_below(m)) & (kQueue - 1)] =
+                    make_uint2((uint32_t)cv[j], ((uint32_t)hv[j] << 24) | (uint32_t)(e - e0));
             const uint32_t nact = (uint32_t)__popcll(m);
             qn += nact;
             qtail += nact;
@@ -266,15 +280,16 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
     };
     if (e1 > e0) {
         float ea[kSuper], eb[kSuper];
+        int32_t ca[kSuper], cb[kSuper];
         uint8_t ha[kSuper], hb[kSuper];
         constexpr int64_t kStep = (int64_t)kSuper * kWave;
-        load_super(e0, ea, ha);
+        load_super(e0, ea, ca, ha);
         for (int64_t s0 = e0; s0 < e1; s0 += 2 * kStep) {
-            load_super(s0 + kStep, eb, hb);
-            scan_super(s0, ea, ha);
+            load_super(s0 + kStep, eb, cb, hb);
+            scan_super(s0, ea, ca, ha);
             if (s0 + kStep >= e1) break;
-            load_super(s0 + 2 * kStep, ea, ha);
-            scan_super(s0 + kStep, eb, hb);
+            load_super(s0 + 2 * kStep, ea, ca, ha);
+            scan_super(s0 + kStep, eb, cb, hb);
         }
     }
     if (qtail != qhead) {
