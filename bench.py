@@ -147,6 +147,26 @@ def copy_probe(torch, U, mb: int = 1024, reps: int = 5) -> float:
     return 2.0 * nbytes / (ms * 1e-3) / 1e9
 
 
+def gather_probe(torch, U, table_bytes: int, reps: int = 3) -> float:
+    """Random 8-byte gathers per second from a table of `table_bytes` (the
+    library's gather probe: the repulsions' access pattern without their
+    arithmetic), on the current stream."""
+    entries = table_bytes // 8
+    table = torch.ones(entries * 2, dtype=torch.float32, device="cuda")
+    threads, iters = 8192 * 256, 8
+    out = torch.empty(threads, dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+    U.umap_probe_gather(table, entries, threads, iters, out, stream)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        U.umap_probe_gather(table, entries, threads, iters, out, stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    return threads * iters * 16 / (ms * 1e-3)
+
+
 def cpu_baseline(w, ids, dist, budget_s: float = 12.0):
     """The C oracle (fp64 push-form Jacobi epochs) timed on the host cores, on
     a sample of epochs spread over the run, from the random initial layout."""
@@ -228,6 +248,12 @@ def main() -> int:
     achieved = bytes_epoch / (launch_ms * 1e-3) / 1e9
     traffic = profiled_traffic(w.name)
     copy_gbps = copy_probe(torch, U)
+    range_bytes = (w.n * w.dim * 4) // st["table_ranges"]
+    table_pow2 = 1 << max(3, (range_bytes - 1).bit_length())
+    gather_range = gather_probe(torch, U, table_pow2)
+    gather_full = gather_probe(torch, U, 1 << max(3, (w.n * w.dim * 4 - 1).bit_length()))
+    # gathers per epoch: a positive sample and neg_rate drawn negatives per sampled edge
+    gathers_per_s = st["edge_updates"] / (epochs_ms * 1e-3)
     gpu_name = torch.cuda.get_device_name(0)
 
     result = {
@@ -264,6 +290,17 @@ def main() -> int:
             "traffic": traffic,
             "algorithmic_bytes_per_launch": bytes_epoch,
             "avg_launch_ms": launch_ms,
+        },
+        "gather_roofline": {
+            "bound": "l2-gather",
+            "achieved": gathers_per_s / 1e9,
+            "peak": gather_range / 1e9,
+            "unit": "G gathers/s",
+            "frac": gathers_per_s / gather_range,
+            "note": f"8-byte vertex gathers of the epoch (one per positive sample and drawn negative) over the "
+                    f"epochs time, against the library's gather probe on a {table_pow2 >> 20} MB table (one "
+                    f"vertex-table range, the slice one repulsion launch gathers from); the probe on the whole "
+                    f"{w.n * w.dim * 4 / 1e6:.0f} MB table reaches {gather_full / 1e9:.0f} G/s",
         },
         "hbm_copy_probe_GBps": copy_gbps,
         "gpu": gpu_name,

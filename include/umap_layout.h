@@ -211,6 +211,15 @@ int umap_fit_ab(float spread, float min_dist, float *a, float *b);
  * `stream` with 16-byte vector loads and stores; not blocking. */
 int umap_probe_copy(const void *src, void *dst, int64_t bytes, void *stream);
 
+/* umap_probe_gather -- random 8-byte gathers: each of `threads` threads (a
+ * positive multiple of 256) reads iters x 16 entries at hashed positions of
+ * `table`, `entries` (a power of two) pairs of fp32 in device memory, the
+ * access pattern of the negative-sample repulsions without their arithmetic.
+ * `out` is device memory for `threads` fp32 (written only so the loads are not
+ * optimised away).  Measures the cache-served gather ceiling of a table of a
+ * given size.  On `stream`; not blocking. */
+int umap_probe_gather(const void *table, int64_t entries, int64_t threads, int32_t iters, void *out, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

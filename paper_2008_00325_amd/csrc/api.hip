@@ -637,4 +637,20 @@ int umap_probe_copy(const void *src, void *dst, int64_t bytes, void *stream)
     }
 }
 
+int umap_probe_gather(const void *table, int64_t entries, int64_t threads, int32_t iters, void *out, void *stream)
+{
+    if (!table || !out) return fail(UMAP_E_INVAL, "table and out must not be NULL");
+    if (entries < 1 || entries > ((int64_t)1 << 32) || (entries & (entries - 1)))
+        return fail(UMAP_E_INVAL, "entries must be a power of two in [1, 2^32]");
+    if (threads < 256 || threads % 256 || threads / 256 > 0x7FFFFFFF)
+        return fail(UMAP_E_INVAL, "threads must be a positive multiple of 256");
+    if (iters < 1) return fail(UMAP_E_INVAL, "iters must be >= 1");
+    try {
+        UL_HIP(ul::launch_probe_gather(table, entries, threads, iters, out, static_cast<hipStream_t>(stream)));
+        return UMAP_OK;
+    } catch (const HipFailure &f) {
+        return hip_fail(f);
+    }
+}
+
 }  // extern "C"

@@ -106,6 +106,8 @@ hipError_t launch_debug_active(const float *eps, int64_t nnz, int32_t epoch, uin
 hipError_t launch_debug_negatives(uint32_t n, uint64_t seed, int32_t epoch, int64_t e_first, int64_t count,
                                   int32_t neg_rate, uint32_t *out, hipStream_t s);
 hipError_t launch_probe_copy(const void *src, void *dst, int64_t bytes, hipStream_t s);
+hipError_t launch_probe_gather(const void *table, int64_t entries, int64_t threads, int32_t iters, void *out,
+                               hipStream_t s);
 
 // ---- fuzzy graph (kernels_graph.hip) ----
 hipError_t launch_fuzzy_graph(int64_t n, int32_t k, const int32_t *ids, const float *dists, int32_t *rows,

@@ -495,25 +495,4 @@ hipError_t launch_debug_negatives(uint32_t n, uint64_t seed, int32_t epoch, int6
     return hipGetLastError();
 }
 
-// ---------------------------------------------------------------------------
-// Roofline probe: a plain 16-byte vector copy.
-// ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_probe_copy(const float4 *__restrict__ src, float4 *__restrict__ dst,
-                                                    int64_t count)
-{
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < count; t += stride) dst[t] = src[t];
-}
-
-hipError_t launch_probe_copy(const void *src, void *dst, int64_t bytes, hipStream_t s)
-{
-    int64_t count = bytes / 16;
-    int64_t blocks = (count + 255) / 256;
-    if (blocks > 256 * 64) blocks = 256 * 64;
-    if (blocks < 1) blocks = 1;
-    hipLaunchKernelGGL(k_probe_copy, dim3((unsigned)blocks), dim3(256), 0, s, (const float4 *)src, (float4 *)dst,
-                       count);
-    return hipGetLastError();
-}
-
 }  // namespace ul

@@ -30,7 +30,7 @@ EXPORTS = (
     "umap_layout_get", "umap_layout_get_device", "umap_layout_set_embedding", "umap_layout_get_graph",
     "umap_layout_stats", "umap_layout_set_stream", "umap_layout_destroy", "umap_layout_last_error",
     "umap_layout_debug_active", "umap_layout_debug_negatives", "umap_layout_set_kernel",
-    "umap_fuzzy_graph_device", "umap_fit_ab", "umap_probe_copy",
+    "umap_fuzzy_graph_device", "umap_fit_ab", "umap_probe_copy", "umap_probe_gather",
 )
 
 
@@ -95,6 +95,7 @@ def lib() -> ctypes.CDLL:
             "umap_fuzzy_graph_device": [i64, i32, P, P, P, P, P, P],
             "umap_fit_ab": [f32, f32, ctypes.POINTER(f32), ctypes.POINTER(f32)],
             "umap_probe_copy": [P, P, i64, P],
+            "umap_probe_gather": [P, i64, i64, i32, P, P],
         }
         for name, args in sig.items():
             fn = getattr(L, name)
@@ -270,3 +271,7 @@ def umap_fit_ab(spread: float = 1.0, min_dist: float = 0.1) -> tuple[float, floa
 
 def umap_probe_copy(src, dst, nbytes: int, stream=None) -> None:
     _check(lib().umap_probe_copy(_dev(src), _dev(dst), nbytes, _stream(stream)))
+
+
+def umap_probe_gather(table, entries: int, threads: int, iters: int, out, stream=None) -> None:
+    _check(lib().umap_probe_gather(_dev(table), entries, threads, iters, _dev(out), _stream(stream)))

@@ -28,7 +28,7 @@ def _declared():
 
 def test_every_declared_function_is_exported(L):
     names = _declared()
-    assert len(names) == 18
+    assert len(names) == 19
     for name in names:
         assert hasattr(L, name), name
         assert name in U.EXPORTS
@@ -104,6 +104,10 @@ def test_fuzzy_graph_and_probe_argument_checks(L):
     assert L.umap_fuzzy_graph_device(10, 5, None, p, p, p, p, None) == U.UMAP_E_INVAL
     assert L.umap_probe_copy(p, p, 17, None) == U.UMAP_E_INVAL
     assert L.umap_probe_copy(None, p, 16, None) == U.UMAP_E_INVAL
+    assert L.umap_probe_gather(p, 3, 256, 1, p, None) == U.UMAP_E_INVAL
+    assert L.umap_probe_gather(p, 4, 100, 1, p, None) == U.UMAP_E_INVAL
+    assert L.umap_probe_gather(p, 4, 256, 0, p, None) == U.UMAP_E_INVAL
+    assert L.umap_probe_gather(None, 4, 256, 1, p, None) == U.UMAP_E_INVAL
 
 
 def test_fit_ab_matches_oracle(orc):

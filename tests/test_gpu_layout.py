@@ -365,3 +365,20 @@ def test_fuzzy_graph_device(which, blobs_graph):
     g = O.prep(n, ro, co, vo.astype(np.float32), 200)
     assert np.array_equal(row_ptr, g.row_ptr) and np.array_equal(col, g.col)
     assert np.allclose(eps, g.eps, rtol=1e-6, atol=0)
+
+
+def test_probes():
+    """The measurement probes run and the copy probe copies."""
+    import torch
+
+    case("copy and gather probes")
+    src = torch.arange(1 << 16, dtype=torch.float32, device="cuda")
+    dst = torch.zeros_like(src)
+    U.umap_probe_copy(src, dst, src.numel() * 4)
+    torch.cuda.synchronize()
+    assert torch.equal(src, dst)
+    table = torch.ones(2 * 4096, dtype=torch.float32, device="cuda")
+    out = torch.zeros(512, dtype=torch.float32, device="cuda")
+    U.umap_probe_gather(table, 4096, 512, 2, out)
+    torch.cuda.synchronize()
+    assert float(out.abs().sum()) == 0.0
