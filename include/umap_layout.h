@@ -181,6 +181,30 @@ int umap_layout_debug_negatives(const umap_layout *h, uint64_t seed, int32_t epo
  * same result bit for bit. */
 int umap_layout_set_kernel(umap_layout *h, int32_t which);
 
+/* ---- quality ------------------------------------------------------------- */
+
+/*
+ * umap_trustworthiness -- T(k) of an embedding on the GPU (the batched pairwise
+ * distance computation of Alg. 1, with the normalisation of Venna and Kaski's
+ * definition that the experiments section cites):
+ *   T(k) = 1 - 2 / (n k (2n - 3k - 1)) sum_i sum_{j in N^_k(i)} max(0, r(i, j) - k),
+ * N^_k(i) the k nearest neighbours of i in the embedding (ties by index),
+ * r(i, j) the 1-based rank of j by input distance from i (self excluded, ties by
+ * index).
+ *   X    n x d fp32 input points, row-major, device memory (read only).
+ *   Y    n x dim fp32 embedding, row-major, device memory (read only), dim 1..16.
+ *   k    1..64, with 2n - 3k - 1 > 0 and n k < 2^31.
+ *   out  host double, receives T.
+ * Distances are fp32 (input distances as |x_i|^2 + |x_j|^2 - 2 x_i . x_j with
+ * the dot products on the matrix cores): a pair closer to a tie than fp32
+ * resolves can rank differently from an exact evaluation, each such pair
+ * moving T by about 1 / (n^2 k).  Errors: UMAP_E_INVAL (arguments, a non-finite
+ * embedding), UMAP_E_NOMEM, UMAP_E_DEVICE.  Scratch of about 8 n k bytes is
+ * allocated on `stream` (NULL: null stream) and freed.  Blocking.
+ */
+int umap_trustworthiness(const float *X, int64_t n, int32_t d, const float *Y, int32_t dim, int32_t k, double *out,
+                         void *stream);
+
 /* ---- input side --------------------------------------------------------- */
 
 /*

@@ -626,6 +626,51 @@ int umap_fuzzy_graph_device(int64_t n, int32_t k, const int32_t *knn_ids, const 
     }
 }
 
+int umap_trustworthiness(const float *X, int64_t n, int32_t d, const float *Y, int32_t dim, int32_t k, double *out,
+                         void *stream)
+{
+    if (!X || !Y || !out) return fail(UMAP_E_INVAL, "X, Y and out must not be NULL");
+    if (n < 1 || n >= ((int64_t)1 << 31)) return fail(UMAP_E_INVAL, "n must be in [1, 2^31), got %lld", (long long)n);
+    if (d < 1) return fail(UMAP_E_INVAL, "d must be >= 1, got %d", d);
+    if (dim < 1 || dim > 16) return fail(UMAP_E_INVAL, "dim must be in [1, 16], got %d", dim);
+    if (k < 1 || k > 64) return fail(UMAP_E_INVAL, "k must be in [1, 64], got %d", k);
+    if (2 * n - 3 * (int64_t)k - 1 <= 0) return fail(UMAP_E_INVAL, "need 2n - 3k - 1 > 0 (n = %lld, k = %d)", (long long)n, k);
+    if (n * (int64_t)k >= ((int64_t)1 << 31)) return fail(UMAP_E_INVAL, "n k must be below 2^31");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    void *scratch = nullptr;
+    try {
+        int ndev = 0;
+        if (hipGetDeviceCount(&ndev) != hipSuccess || ndev < 1) return fail(UMAP_E_DEVICE, "no HIP device available");
+        const size_t nk = (size_t)n * (size_t)k;
+        size_t bytes = need<float>(n) + need<int32_t>(nk) + need<float>(nk) + need<int64_t>(n) +
+                       need<unsigned long long>(1) + need<unsigned>(1);
+        UL_HIP(hipMallocAsync(&scratch, bytes, s));
+        Carver cv{static_cast<char *>(scratch)};
+        float *nx = cv.take<float>(n);
+        int32_t *nbr = cv.take<int32_t>(nk);
+        float *thr = cv.take<float>(nk);
+        int64_t *pen = cv.take<int64_t>(n);
+        unsigned long long *sum = cv.take<unsigned long long>(1);
+        unsigned *flags = cv.take<unsigned>(1);
+        UL_HIP(hipMemsetAsync(flags, 0, sizeof(unsigned), s));
+        UL_HIP(ul::launch_trustworthiness(X, n, d, Y, dim, k, nx, nbr, thr, pen, sum, flags, s));
+        unsigned long long hsum = 0;
+        unsigned hflags = 0;
+        UL_HIP(hipMemcpyAsync(&hsum, sum, sizeof hsum, hipMemcpyDeviceToHost, s));
+        UL_HIP(hipMemcpyAsync(&hflags, flags, sizeof hflags, hipMemcpyDeviceToHost, s));
+        UL_HIP(hipFreeAsync(scratch, s));
+        scratch = nullptr;
+        UL_HIP(hipStreamSynchronize(s));
+        if (hflags) return fail(UMAP_E_INVAL, "the embedding has non-finite coordinates");
+        const double nn = (double)n, kk = (double)k;
+        *out = 1.0 - 2.0 / (nn * kk * (2.0 * nn - 3.0 * kk - 1.0)) * (double)hsum;
+        return UMAP_OK;
+    } catch (const HipFailure &f) {
+        if (scratch) hipFreeAsync(scratch, s);
+        return hip_fail(f);
+    }
+}
+
 int umap_probe_copy(const void *src, void *dst, int64_t bytes, void *stream)
 {
     if (!src || !dst || bytes < 0 || bytes % 16) return fail(UMAP_E_INVAL, "need non-NULL pointers and bytes % 16 == 0");

@@ -31,6 +31,7 @@ EXPORTS = (
     "umap_layout_stats", "umap_layout_set_stream", "umap_layout_destroy", "umap_layout_last_error",
     "umap_layout_debug_active", "umap_layout_debug_negatives", "umap_layout_set_kernel",
     "umap_fuzzy_graph_device", "umap_fit_ab", "umap_probe_copy", "umap_probe_gather",
+    "umap_trustworthiness",
 )
 
 
@@ -96,6 +97,7 @@ def lib() -> ctypes.CDLL:
             "umap_fit_ab": [f32, f32, ctypes.POINTER(f32), ctypes.POINTER(f32)],
             "umap_probe_copy": [P, P, i64, P],
             "umap_probe_gather": [P, i64, i64, i32, P, P],
+            "umap_trustworthiness": [P, i64, i32, P, i32, i32, ctypes.POINTER(ctypes.c_double), P],
         }
         for name, args in sig.items():
             fn = getattr(L, name)
@@ -271,6 +273,17 @@ def umap_fit_ab(spread: float = 1.0, min_dist: float = 0.1) -> tuple[float, floa
 
 def umap_probe_copy(src, dst, nbytes: int, stream=None) -> None:
     _check(lib().umap_probe_copy(_dev(src), _dev(dst), nbytes, _stream(stream)))
+
+
+def umap_trustworthiness(X, Y, k: int, stream=None) -> float:
+    """T(k) of embedding Y (n x dim) of points X (n x d); both device tensors (fp32, contiguous)."""
+    n, d = int(X.shape[0]), int(X.shape[1])
+    dim = int(Y.shape[1])
+    if int(Y.shape[0]) != n:
+        raise ValueError("X and Y need the same number of rows")
+    out = ctypes.c_double()
+    _check(lib().umap_trustworthiness(_dev(X), n, d, _dev(Y), dim, k, ctypes.byref(out), _stream(stream)))
+    return out.value
 
 
 def umap_probe_gather(table, entries: int, threads: int, iters: int, out, stream=None) -> None:

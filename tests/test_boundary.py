@@ -28,7 +28,7 @@ def _declared():
 
 def test_every_declared_function_is_exported(L):
     names = _declared()
-    assert len(names) == 19
+    assert len(names) == 20
     for name in names:
         assert hasattr(L, name), name
         assert name in U.EXPORTS
@@ -108,6 +108,13 @@ def test_fuzzy_graph_and_probe_argument_checks(L):
     assert L.umap_probe_gather(p, 4, 100, 1, p, None) == U.UMAP_E_INVAL
     assert L.umap_probe_gather(p, 4, 256, 0, p, None) == U.UMAP_E_INVAL
     assert L.umap_probe_gather(None, 4, 256, 1, p, None) == U.UMAP_E_INVAL
+    out = ctypes.c_double(7.0)
+    for n, d, dim, k in [(0, 4, 2, 1), (100, 0, 2, 15), (100, 4, 0, 15), (100, 4, 17, 15), (100, 4, 2, 0),
+                         (100, 4, 2, 65), (22, 4, 2, 15)]:
+        assert L.umap_trustworthiness(p, n, d, p, dim, k, ctypes.byref(out), None) == U.UMAP_E_INVAL
+    assert L.umap_trustworthiness(None, 100, 4, p, 2, 15, ctypes.byref(out), None) == U.UMAP_E_INVAL
+    assert L.umap_trustworthiness(p, 100, 4, p, 2, 15, None, None) == U.UMAP_E_INVAL
+    assert out.value == 7.0
 
 
 def test_fit_ab_matches_oracle(orc):

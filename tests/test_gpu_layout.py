@@ -26,6 +26,16 @@ TOL = 1e-4
 A_DEF, B_DEF = 1.5769434, 0.8950608
 
 
+@pytest.fixture(scope="module", autouse=True)
+def torch_device_first():
+    """Initialise torch's HIP runtime before the library's (torch ships its own
+    copy of the runtime; the tests use torch tensors for device memory)."""
+    import torch
+
+    torch.cuda.init()
+    torch.cuda.set_device(0)
+
+
 def case(msg):
     print(f"[gpu case] {msg}", flush=True)
     sys.stdout.flush()
@@ -382,3 +392,113 @@ def test_probes():
     U.umap_probe_gather(table, 4096, 512, 2, out)
     torch.cuda.synchronize()
     assert float(out.abs().sum()) == 0.0
+
+
+# ---------------------------------------------------------------------------
+# quality: trustworthiness on the GPU (Alg. 1) against the oracle's
+# ---------------------------------------------------------------------------
+
+# a rank decided differently by fp32 than by the oracle's fp64 (a pair of input
+# distances closer than fp32 resolves) moves T by 2 / (n k (2n - 3k - 1)) per unit
+TW_TOL = 2e-6
+
+
+@pytest.mark.parametrize("k", [5, 15, 50])
+def test_trustworthiness_blobs(blobs_graph, k):
+    import torch
+
+    w, X, ids, dist, _ = blobs_graph
+    rng = np.random.default_rng(k)
+    for label, Y in [("pca-like", X[:, :2].copy()), ("noise", rng.normal(size=(w.n, 2)).astype(np.float32)),
+                     ("3-d", (X[:, :3] + 0.5 * rng.normal(size=(w.n, 3))).astype(np.float32))]:
+        case(f"trustworthiness blobs2k k={k} {label}")
+        tg = U.umap_trustworthiness(torch.from_numpy(X).cuda(), torch.from_numpy(Y).cuda(), k)
+        to = O.trustworthiness(X, Y, k)
+        print(f"  T(gpu) = {tg:.9f}  T(oracle) = {to:.9f}  diff = {tg - to:.2e}", flush=True)
+        assert abs(tg - to) <= TW_TOL
+
+
+def test_trustworthiness_ragged_shapes():
+    """n not a multiple of the 64-point tiles, d not a multiple of the 16-feature
+    chunks, an identity embedding (T = 1), and a one-dimensional embedding."""
+    import torch
+
+    rng = np.random.default_rng(5)
+    n, d = 3001, 37
+    X = rng.normal(size=(n, d)).astype(np.float32)
+    Xg = torch.from_numpy(X).cuda()
+    case("trustworthiness identity n=3001 d=37")
+    # the embedding equal to the input in a subspace it is ranked by: T = 1
+    Z = np.zeros((n, 16), np.float32)
+    Z[:, :16] = X[:, :16]
+    X16 = np.zeros_like(X)
+    X16[:, :16] = X[:, :16]
+    t_id = U.umap_trustworthiness(torch.from_numpy(X16).cuda(), torch.from_numpy(Z).cuda(), 15)
+    assert 1.0 - TW_TOL <= t_id <= 1.0
+    for dim in (1, 2):
+        case(f"trustworthiness n=3001 d=37 dim={dim}")
+        Y = (X[:, :dim] + 0.2 * rng.normal(size=(n, dim))).astype(np.float32)
+        tg = U.umap_trustworthiness(Xg, torch.from_numpy(Y).cuda(), 15)
+        to = O.trustworthiness(X, Y, 15)
+        print(f"  T(gpu) = {tg:.9f}  T(oracle) = {to:.9f}", flush=True)
+        assert abs(tg - to) <= TW_TOL
+    case("trustworthiness rejects a non-finite embedding")
+    Y = rng.normal(size=(n, 2)).astype(np.float32)
+    Y[7, 1] = np.nan
+    with pytest.raises(U.UmapLayoutError) as ei:
+        U.umap_trustworthiness(Xg, torch.from_numpy(Y).cuda(), 15)
+    assert ei.value.code == U.UMAP_E_INVAL
+
+
+def _knn_torch(X, k, batch=4096):
+    """Exact Euclidean kNN (self excluded) of the rows of X with torch on the
+    GPU: the input preparation of the image-like workload (its 70,000 x 784
+    distance matrix is too slow for a numpy test).  Both layouts below are run
+    on the same lists, so these serve as their common input."""
+    import torch
+
+    Xg = torch.from_numpy(X).cuda()
+    sq = (Xg * Xg).sum(1)
+    n = X.shape[0]
+    ids = np.empty((n, k), np.int32)
+    dist = np.empty((n, k), np.float32)
+    for s in range(0, n, batch):
+        t = min(n, s + batch)
+        D = sq[s:t, None] + sq[None, :] - 2.0 * (Xg[s:t] @ Xg.T)
+        D[torch.arange(t - s), torch.arange(s, t)] = float("inf")
+        d, i = torch.topk(D, k, dim=1, largest=False, sorted=True)
+        ids[s:t] = i.int().cpu().numpy()
+        dist[s:t] = torch.sqrt(torch.clamp(d, min=0.0)).cpu().numpy()
+    return ids, dist
+
+
+def test_full_run_trustworthiness_image70k():
+    """The image-like workload at full size (70,000 x 784, 10 clusters, k = 15,
+    200 epochs): T@15 of the GPU layout within 0.01 of the oracle's layout, both
+    scored by the GPU trustworthiness (pinned against the oracle's above)."""
+    import torch
+
+    w = synth.WORKLOADS["image70k"]
+    case("image70k: points and kNN")
+    X, _ = synth.workload_points(w)
+    ids, dist = _knn_torch(X, w.k)
+    r, c, v = O.fuzzy_graph(ids, dist)
+    a, b = O.fit_ab(w.spread, w.min_dist)
+    g = O.prep(w.n, r, c, v, w.n_epochs)
+    seed = 3
+    case("image70k: GPU layout")
+    with U.umap_layout_create(w.n, w.dim, r, c, v, a, b, w.n_epochs, w.neg_rate) as h:
+        _check_graph(h, g)
+        U.umap_layout_run(h, seed)
+        Eg = U.umap_layout_get(h)
+        st = U.umap_layout_stats(h)
+    case("image70k: oracle layout")
+    Eo, act = O.run(g, w.dim, a, b, w.n_epochs, w.neg_rate, seed)
+    assert st["active_edges"] == int(act.sum())
+    assert np.all(np.isfinite(Eg))
+    case("image70k: trustworthiness of both")
+    Xg = torch.from_numpy(X).cuda()
+    tg = U.umap_trustworthiness(Xg, torch.from_numpy(Eg).cuda(), 15)
+    to = U.umap_trustworthiness(Xg, torch.from_numpy(Eo.astype(np.float32)).cuda(), 15)
+    print(f"  T@15(gpu layout) = {tg:.5f}  T@15(oracle layout) = {to:.5f}", flush=True)
+    assert abs(tg - to) <= 0.01
