@@ -67,6 +67,10 @@ typedef struct {
     int32_t table_ranges;   /* P: an epoch is one draw launch and P repulsion
                                launches, each gathering from 1/P of the table   */
     int32_t kernel;         /* epoch kernel in use (see umap_layout_set_kernel)  */
+    int32_t overflow_redone; /* 1 when the last call's epochs were redone by the
+                               one-thread-per-vertex kernel because a negative
+                               sample found its record slot full (the result is
+                               the same bit for bit; only the time is lost)    */
 } umap_layout_stats_t;
 
 /*

@@ -52,11 +52,19 @@ int hip_fail(const HipFailure &f)
 
 // Optional failure injection for tests: UMAP_LAYOUT_FAULT=alloc makes the
 // arena allocation report out-of-memory; UMAP_LAYOUT_FAULT=launch@K makes the
-// launch of epoch K report a device error.  Nothing is launched in either case.
+// launch of epoch K report a device error (nothing is launched in either
+// case); UMAP_LAYOUT_FAULT=records gives the wavefront kernel no record slots,
+// so every negative sample overflows and the epochs are redone.
 bool fault_alloc()
 {
     const char *f = getenv("UMAP_LAYOUT_FAULT");
     return f && strcmp(f, "alloc") == 0;
+}
+
+bool fault_records()
+{
+    const char *f = getenv("UMAP_LAYOUT_FAULT");
+    return f && strcmp(f, "records") == 0;
 }
 
 int fault_launch_epoch()
@@ -131,7 +139,9 @@ struct umap_layout {
     unsigned long long *active = nullptr;   // n_epochs sampled-edge counts
     int32_t *counts = nullptr;              // ring of per-wave counts
     int32_t lg_phases = 0;                  // negative samples split over 2^lg table ranges
-    uint32_t *rec = nullptr;                // records of negative samples, per range
+    uint32_t *rec = nullptr;                // records of negative samples, slots by record_offset
+    unsigned *overflow = nullptr;           // raised when a record slot was full
+    float *E_start = nullptr;               // layout at the start of a call, for a redo
     int32_t *rec_count = nullptr;           // per range and wave
     long long *delta = nullptr;             // fixed-point partial sums between launches
     int64_t count_stride = 0;               // slots per ring row
@@ -186,8 +196,9 @@ int create_common(umap_layout **out, int64_t n, int32_t dim, const int32_t *rows
         size_t bytes = need<int64_t>(n + 1) + need<int32_t>(nnz) + need<float>(nnz) + need<int32_t>(max_waves + 1) +
                        2 * need<float>(nd) + need<unsigned long long>(n_epochs) + need<uint8_t>(nnz) +
                        need<int32_t>((size_t)count_rows * count_stride) +
-                       need<uint32_t>((size_t)n_phases * neg_rate * nnz) + need<int32_t>((size_t)n_phases * max_waves) +
-                       need<long long>(nd);
+                       need<uint32_t>(ul::record_offset(max_waves, nnz, neg_rate, (int32_t)n_phases)) +
+                       need<int32_t>((size_t)n_phases * max_waves) + need<long long>(nd) + need<unsigned>(1) +
+                       need<float>(nd);
         if (fault_alloc()) throw HipFailure{hipErrorOutOfMemory, "hipMalloc(arena) [injected]"};
         UL_HIP(hipMalloc(&h->arena, bytes));
         Carver cv{static_cast<char *>(h->arena)};
@@ -202,9 +213,11 @@ int create_common(umap_layout **out, int64_t n, int32_t dim, const int32_t *rows
         h->counts = cv.take<int32_t>((size_t)count_rows * count_stride);
         h->count_stride = count_stride;
         h->lg_phases = lg_phases;
-        h->rec = cv.take<uint32_t>((size_t)n_phases * neg_rate * nnz);
+        h->rec = cv.take<uint32_t>(ul::record_offset(max_waves, nnz, neg_rate, (int32_t)n_phases));
         h->rec_count = cv.take<int32_t>((size_t)n_phases * max_waves);
         h->delta = cv.take<long long>(nd);
+        h->overflow = cv.take<unsigned>(1);
+        h->E_start = cv.take<float>(nd);
 
         // ingest scratch (stream-ordered)
         ul::PrepBuffers B{};
@@ -308,11 +321,10 @@ int run_epochs_impl(umap_layout *h, uint64_t seed, int32_t first, int32_t last, 
     A.b = h->b;
     A.key_lo = (uint32_t)seed;
     A.key_hi = (uint32_t)(seed >> 32);
-    ul::WaveGraph G{h->row_ptr, h->col,      h->eps,      h->head,     h->part,
-                    h->n_waves,  1 << h->lg_phases,
-                    h->lg_phases, h->rec,     (int64_t)h->neg_rate * h->nnz, h->rec_count, h->delta};
-    UL_HIP(ul::launch_zero_u64(h->active, h->n_epochs, h->stream));
-    UL_HIP(hipEventRecord(h->ev[1], h->stream));
+    ul::WaveGraph G{h->row_ptr,     h->col,       h->eps,    h->head,      h->part,
+                    h->n_waves,     1 << h->lg_phases,       h->lg_phases, h->rec,
+                    h->rec_count,   h->overflow,  fault_records() ? (int64_t)0 : (int64_t)-1,
+                    h->delta};
     // the wave kernels store a sample's offset inside its table range and a
     // sampled edge's offset inside its wave in 24 bits (a wave holds fewer
     // than kWaveCost + max_degree edges); beyond that (n >= 2^28 vertices, or
@@ -320,25 +332,59 @@ int run_epochs_impl(umap_layout *h, uint64_t seed, int32_t first, int32_t last, 
     const bool fits = (h->n >> h->lg_phases) + 2 < ((int64_t)1 << 24) &&
                       (int64_t)h->max_degree + ul::kWaveCost < ((int64_t)1 << 24);
     const int kernel = fits ? h->kernel : 1;
-    const int64_t slots = ul::count_slots(kernel, h->n, h->n_waves);
-    const int ring = h->n_epochs < ul::kCountRing ? h->n_epochs : ul::kCountRing;
-    int32_t pending_from = first;   // first epoch whose counts are not yet summed
-    for (int32_t ep = first; ep < last; ++ep) {
-        if (ep == fault) {
-            UL_HIP(hipStreamSynchronize(h->stream));
-            return fail(UMAP_E_DEVICE, "epoch %d launch failed [injected]", ep);
+    const bool records = kernel != 1;
+    const int cur0 = h->cur;
+    const size_t nd_bytes = sizeof(float) * (size_t)h->n * (size_t)h->dim;
+    if (records) {
+        // the layout this call starts from, in case a record slot overflows
+        UL_HIP(hipMemsetAsync(h->overflow, 0, sizeof(unsigned), h->stream));
+        UL_HIP(hipMemcpyAsync(h->E_start, h->E[cur0], nd_bytes, hipMemcpyDeviceToDevice, h->stream));
+    }
+    UL_HIP(hipEventRecord(h->ev[1], h->stream));
+
+    // epochs [first, last) with one kernel; fault >= 0 injects a launch error
+    auto epochs = [&](int which) -> int {
+        UL_HIP(ul::launch_zero_u64(h->active, h->n_epochs, h->stream));
+        const int64_t slots = ul::count_slots(which, h->n, h->n_waves);
+        const int ring = h->n_epochs < ul::kCountRing ? h->n_epochs : ul::kCountRing;
+        int32_t pending_from = first;   // first epoch whose counts are not yet summed
+        for (int32_t ep = first; ep < last; ++ep) {
+            if (ep == fault) {
+                UL_HIP(hipStreamSynchronize(h->stream));
+                return fail(UMAP_E_DEVICE, "epoch %d launch failed [injected]", ep);
+            }
+            A.E = h->E[h->cur];
+            A.E_next = h->E[1 - h->cur];
+            A.epoch = ep;
+            A.alpha = 1.0 - (double)ep / (double)h->n_epochs;
+            A.counts = h->counts + (int64_t)((ep - pending_from) % ring) * h->count_stride;
+            UL_HIP(ul::launch_epoch(which, h->dim, A, G, h->stream));
+            h->cur = 1 - h->cur;
+            if (ep + 1 - pending_from == ring || ep + 1 == last) {
+                UL_HIP(ul::launch_reduce_counts(h->counts, h->count_stride, slots, ep + 1 - pending_from,
+                                                h->active + pending_from, h->stream));
+                pending_from = ep + 1;
+            }
         }
-        A.E = h->E[h->cur];
-        A.E_next = h->E[1 - h->cur];
-        A.epoch = ep;
-        A.alpha = 1.0 - (double)ep / (double)h->n_epochs;
-        A.counts = h->counts + (int64_t)((ep - pending_from) % ring) * h->count_stride;
-        UL_HIP(ul::launch_epoch(kernel, h->dim, A, G, h->stream));
-        h->cur = 1 - h->cur;
-        if (ep + 1 - pending_from == ring || ep + 1 == last) {
-            UL_HIP(ul::launch_reduce_counts(h->counts, h->count_stride, slots, ep + 1 - pending_from,
-                                            h->active + pending_from, h->stream));
-            pending_from = ep + 1;
+        return UMAP_OK;
+    };
+
+    int rc = epochs(kernel);
+    if (rc != UMAP_OK) return rc;
+    h->st.overflow_redone = 0;
+    if (records) {
+        unsigned overflow = 0;
+        UL_HIP(hipMemcpyAsync(&overflow, h->overflow, sizeof overflow, hipMemcpyDeviceToHost, h->stream));
+        UL_HIP(hipStreamSynchronize(h->stream));
+        if (overflow) {
+            // a range slot was full: some negative samples were not applied;
+            // redo the call's epochs from its starting layout with the
+            // one-thread-per-vertex kernel, which keeps no records
+            h->cur = cur0;
+            UL_HIP(hipMemcpyAsync(h->E[cur0], h->E_start, nd_bytes, hipMemcpyDeviceToDevice, h->stream));
+            rc = epochs(1);
+            if (rc != UMAP_OK) return rc;
+            h->st.overflow_redone = 1;
         }
     }
     UL_HIP(hipEventRecord(h->ev[2], h->stream));

@@ -80,11 +80,23 @@ struct WaveGraph {
     // negative samples are filed by vertex-table range: P = 2^lg_phases ranges
     int32_t n_phases;
     int32_t lg_phases;
-    uint32_t *rec;            // P x rec_stride records ((row in wave) << 24 | offset in range)
-    int64_t rec_stride;       // neg_rate x kept edges: wave w's slice starts at neg_rate x e0
+    uint32_t *rec;            // records ((row in wave) << 24 | offset in range), slots by record_offset
     int32_t *rec_count;       // P x n_waves
+    unsigned *overflow;       // set when a record did not fit its range slot
+    int64_t cap_limit;        // < 0: none; else record slots per range are cut to it (failure injection)
     long long *delta;         // n x dim fixed-point partial sums between launches
 };
+
+// First record slot of wave w (edges from e0): every wave gets
+// 1.25 x neg_rate x its edges + 256 x P slots, split evenly over the P table
+// ranges.  A range of a wave gets more than its share of a wave's draws only
+// with vanishing probability (the ranges split uniform random words); a draw
+// that finds its range full raises the overflow flag and the epochs are redone
+// by the one-thread-per-vertex kernel.
+__host__ __device__ inline int64_t record_offset(int64_t w, int64_t e0, int32_t neg_rate, int32_t n_phases)
+{
+    return (5 * (int64_t)neg_rate * e0 + 3) / 4 + (int64_t)256 * n_phases * w;
+}
 
 // At most this many table ranges (phases) per epoch.
 constexpr int kMaxPhases = 16;

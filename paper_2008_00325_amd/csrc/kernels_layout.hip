@@ -206,7 +206,10 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
     };
     const int32_t R = A.neg_rate;
     const int32_t lg = G.lg_phases;
-    uint32_t *const rec_wave = G.rec + (int64_t)R * e0;   // this wave's slice of every range
+    const int64_t roff = record_offset(w, e0, R, G.n_phases);
+    int64_t cap = (record_offset(w + 1, e1, R, G.n_phases) - roff) / G.n_phases;   // slots per range
+    if (G.cap_limit >= 0 && cap > G.cap_limit) cap = G.cap_limit;
+    uint32_t *const rec_wave = G.rec + roff;   // this wave's slots, range p from p * cap
     uint2 *q = s_q[wv];
     uint32_t qhead = 0, qtail = 0;
     auto file = [&](uint32_t u, uint32_t i, int h) {
@@ -214,7 +217,8 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
         if (k == i) return;   // a draw equal to the source adds nothing
         const uint32_t p = lg == 0 ? 0u : u >> (32 - lg);
         const uint32_t slot = atomicAdd(&rec_n[p], 1u);
-        rec_wave[(int64_t)p * G.rec_stride + slot] = ((uint32_t)h << 24) | (k - range_base(p, lg, A.n));
+        if (slot < cap) rec_wave[(int64_t)p * cap + slot] = ((uint32_t)h << 24) | (k - range_base(p, lg, A.n));
+        else atomicOr(G.overflow, 1u);
     };
     // attraction and negative draws of `count` queued sampled edges
     auto process = [&](int count) {
@@ -320,7 +324,12 @@ __global__ __launch_bounds__(256) void k_epoch_repulse(EpochArgs A, WaveGraph G,
     const int nrows = __builtin_amdgcn_readfirstlane(G.part[w + 1]) - (int)r0;
     if (nrows <= 0) return;
     const int64_t e0 = uniform64(G.row_ptr[r0]);
-    const int64_t nrec = __builtin_amdgcn_readfirstlane(G.rec_count[(int64_t)phase * G.n_waves + w]);
+    const int64_t e1 = uniform64(G.row_ptr[r0 + nrows]);
+    const int64_t roff = record_offset(w, e0, A.neg_rate, G.n_phases);
+    int64_t cap = (record_offset(w + 1, e1, A.neg_rate, G.n_phases) - roff) / G.n_phases;
+    if (G.cap_limit >= 0 && cap > G.cap_limit) cap = G.cap_limit;
+    int64_t nrec = __builtin_amdgcn_readfirstlane(G.rec_count[(int64_t)phase * G.n_waves + w]);
+    nrec = nrec < cap ? nrec : cap;
     const bool last = phase + 1 == G.n_phases;
 
     long long *acc = s_acc[wv];
@@ -332,7 +341,7 @@ __global__ __launch_bounds__(256) void k_epoch_repulse(EpochArgs A, WaveGraph G,
     }
     wave_sync();
 
-    const uint32_t *recs = G.rec + (int64_t)A.neg_rate * e0 + (int64_t)phase * G.rec_stride;
+    const uint32_t *recs = G.rec + roff + (int64_t)phase * cap;
     const uint32_t base = range_base((uint32_t)phase, G.lg_phases, A.n);
     // kRepUnroll records per lane per step, all loads issued before use
     for (int64_t b = 0; b < nrec; b += kRepUnroll * kWave) {

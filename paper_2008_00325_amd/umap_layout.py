@@ -53,6 +53,7 @@ class umap_layout_stats_t(ctypes.Structure):
         ("epochs_ms", ctypes.c_double),
         ("table_ranges", ctypes.c_int32),
         ("kernel", ctypes.c_int32),
+        ("overflow_redone", ctypes.c_int32),
     ]
 
     def as_dict(self) -> dict:

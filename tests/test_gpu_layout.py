@@ -203,7 +203,9 @@ def _epoch_parity(h, g, E, epochs, a, b, N, R, seed, label):
         err = float(np.abs(got.astype(np.float64) - ref).max())
         print(f"  max|diff| = {err:.3e}  active = {act}", flush=True)
         assert err <= TOL
-        assert U.umap_layout_stats(h)["active_edges"] == act
+        st = U.umap_layout_stats(h)
+        assert st["active_edges"] == act
+        assert st["overflow_redone"] == 0
 
 
 def test_single_epoch_blobs(blobs_graph):
@@ -240,6 +242,34 @@ def test_single_epoch_window1m_full_size(window1m_graph):
             E = synth.embedding_state(w.n, w.dim, seed, scale)
             _epoch_parity(h, g, E, (0, 1, w.n_epochs // 2, w.n_epochs - 1), a, b, w.n_epochs, w.neg_rate, 11,
                           f"window1m scale {scale}")
+
+
+@pytest.mark.parametrize("name", ["window1m_k30", "window5m"])
+def test_single_epoch_other_full_sizes(name):
+    """The two other full-size workloads: 1M vertices with k = 30 in 3-D (8
+    table ranges) and 5M vertices with lognormal cluster sizes (16 table
+    ranges); whole layout compared after one epoch fed the same fp32 state."""
+    import torch
+
+    w = synth.WORKLOADS[name]
+    case(f"{name}: building the graph on the host")
+    ids, dist = synth.workload_knn(w)
+    r, c, v = O.fuzzy_graph(ids, dist)
+    del ids, dist
+    g = O.prep(w.n, r, c, v, w.n_epochs)
+    a, b = O.fit_ab(w.spread, w.min_dist)
+    dr, dc, dv = (torch.from_numpy(x).cuda() for x in (r, c, v))
+    nnz = r.size
+    del r, c, v
+    with U.umap_layout_create_device(w.n, w.dim, dr, dc, dv, nnz, a, b, w.n_epochs, w.neg_rate) as h:
+        del dr, dc, dv
+        _check_graph(h, g)
+        st = U.umap_layout_stats(h)
+        case(f"{name}: {st['table_ranges']} table ranges, {st['nnz_kept']} edges")
+        assert st["table_ranges"] == (8 if w.dim == 3 else 16)
+        E = synth.embedding_state(w.n, w.dim, 6, 10.0)
+        _epoch_parity(h, g, E, (0, 1, w.n_epochs // 2, w.n_epochs - 1), a, b, w.n_epochs, w.neg_rate, 13,
+                      f"{name} scale 10")
 
 
 @pytest.mark.parametrize("dim,R,N", [(1, 5, 20), (3, 5, 200), (4, 0, 50), (16, 7, 30)])
@@ -337,6 +367,38 @@ def test_fault_injection(monkeypatch, blobs_graph):
         with pytest.raises(U.UmapLayoutError) as ei:
             U.umap_layout_run_epochs(h, 1, 0, 1)
         assert ei.value.code == U.UMAP_E_STATE
+
+
+def test_record_overflow_redo(monkeypatch, window1m_graph):
+    """A negative sample that finds its record slot full raises a flag, and the
+    call's epochs are redone from the layout the call started from by the
+    one-thread-per-vertex kernel: the result is the same bit for bit.  Failure
+    injection gives the wavefront kernel no record slots at all."""
+    w, ids, dist, (r, c, v) = window1m_graph
+    E0 = synth.embedding_state(w.n, w.dim, 21, 10.0)
+    case("record overflow redo, window1m, epochs 0..3 then 3..5")
+    with U.umap_layout_create(w.n, w.dim, r, c, v, A_DEF, B_DEF, w.n_epochs, w.neg_rate) as h:
+        assert U.umap_layout_stats(h)["table_ranges"] > 1
+        U.umap_layout_set_embedding(h, E0)
+        U.umap_layout_run_epochs(h, 9, 0, 3)
+        st = U.umap_layout_stats(h)
+        assert st["overflow_redone"] == 0
+        ref3, act3 = U.umap_layout_get(h), st["active_edges"]
+        U.umap_layout_run_epochs(h, 9, 3, 5)
+        ref5 = U.umap_layout_get(h)
+
+        monkeypatch.setenv("UMAP_LAYOUT_FAULT", "records")
+        U.umap_layout_set_embedding(h, E0)
+        U.umap_layout_run_epochs(h, 9, 0, 3)
+        st = U.umap_layout_stats(h)
+        assert st["overflow_redone"] == 1 and st["active_edges"] == act3
+        assert np.array_equal(U.umap_layout_get(h).view(np.uint32), ref3.view(np.uint32))
+        U.umap_layout_run_epochs(h, 9, 3, 5)
+        assert U.umap_layout_stats(h)["overflow_redone"] == 1
+        assert np.array_equal(U.umap_layout_get(h).view(np.uint32), ref5.view(np.uint32))
+        monkeypatch.delenv("UMAP_LAYOUT_FAULT")
+        U.umap_layout_run_epochs(h, 9, 0, 1)
+        assert U.umap_layout_stats(h)["overflow_redone"] == 0
 
 
 # ---------------------------------------------------------------------------
