@@ -129,6 +129,28 @@ def gpu_steps(w, torch, U, coo, a, b, steps: int, warmup: int):
     return stats, wall, ok
 
 
+def async_mode(w, torch, U, coo, a, b, reps: int = 3) -> dict:
+    """The asynchronous (Hogwild) mode on the same input, outside the timed
+    steps: median device time of the epochs over `reps` runs."""
+    rows, cols, vals = coo
+    with U.umap_layout_create_device(w.n, w.dim, rows, cols, vals, rows.numel(), a, b, w.n_epochs, w.neg_rate) as h:
+        U.umap_layout_set_mode(h, U.UMAP_MODE_ASYNC)
+        runs = []
+        for s in range(reps):
+            U.umap_layout_run(h, 2000 + s)
+            runs.append(U.umap_layout_stats(h))
+        finite = bool(np.isfinite(U.umap_layout_get(h)).all())
+    ms = float(np.median([r["epochs_ms"] for r in runs]))
+    log(f"asynchronous mode: epochs {ms:.2f} ms (median of {reps})")
+    return {
+        "epochs_ms": ms,
+        "edge_updates_per_s": runs[-1]["edge_updates"] / (ms * 1e-3),
+        "finite": finite,
+        "note": "asynchronous in-place (Hogwild) updates, one launch per epoch; not bit-repeatable, quality "
+                "checked by the tests (trustworthiness within 0.01 of the oracle's)",
+    }
+
+
 def copy_probe(torch, U, mb: int = 1024, reps: int = 5) -> float:
     """HBM copy bandwidth of the library's plain 16-byte copy kernel (GB/s,
     read + write bytes), on the current stream."""
@@ -247,6 +269,7 @@ def main() -> int:
     launch_ms = epochs_ms / n_epochs
     achieved = bytes_epoch / (launch_ms * 1e-3) / 1e9
     traffic = profiled_traffic(w.name)
+    async_stats = async_mode(w, torch, U, (rows, cols, vals), a, b)
     copy_gbps = copy_probe(torch, U)
     range_bytes = (w.n * w.dim * 4) // st["table_ranges"]
     table_pow2 = 1 << max(3, (range_bytes - 1).bit_length())
@@ -302,6 +325,7 @@ def main() -> int:
                     f"vertex-table range, the slice one repulsion launch gathers from); the probe on the whole "
                     f"{w.n * w.dim * 4 / 1e6:.0f} MB table reaches {gather_full / 1e9:.0f} G/s",
         },
+        "async_mode": async_stats,
         "hbm_copy_probe_GBps": copy_gbps,
         "gpu": gpu_name,
     }

@@ -12,10 +12,12 @@
  * source away (gradient of log(1 - Phi)); embedding-updates section.  Edge e
  * of weight w_e is sampled once every eps_e = w_max / w_e epochs.  Gradient
  * components are clipped to [-4, 4]; the step size decays linearly,
- * alpha_n = 1 - n / n_epochs.  Updates are epoch-synchronous: every read of
- * epoch n sees the layout at the start of the epoch and all updates are applied
- * at its end, which makes the result a deterministic function of the seed
- * (the exactly-repeatable mode of the reproducibility section).
+ * alpha_n = 1 - n / n_epochs.  By default updates are epoch-synchronous:
+ * every read of epoch n sees the layout at the start of the epoch and all
+ * updates are applied at its end, which makes the result a deterministic
+ * function of the seed (the exactly-repeatable mode of the reproducibility
+ * section).  umap_layout_set_mode selects the asynchronous (Hogwild) mode
+ * instead, the paper's default: updates land in place while the epoch runs.
  *
  * Conventions.
  *   - Every function returns UMAP_OK (0) or a negative UMAP_E_* code and, on
@@ -46,6 +48,9 @@ extern "C" {
 #define UMAP_E_DEVICE (-4)     /* no usable GPU, or a HIP call failed          */
 #define UMAP_E_STATE (-5)      /* call not valid in the handle's current state */
 
+#define UMAP_MODE_SYNC 0       /* epoch-synchronous updates (default)          */
+#define UMAP_MODE_ASYNC 1      /* asynchronous in-place updates (Hogwild)      */
+
 typedef struct umap_layout umap_layout;
 
 typedef struct {
@@ -71,6 +76,7 @@ typedef struct {
                                one-thread-per-vertex kernel because a negative
                                sample found its record slot full (the result is
                                the same bit for bit; only the time is lost)    */
+    int32_t mode;           /* UMAP_MODE_SYNC or UMAP_MODE_ASYNC                 */
 } umap_layout_stats_t;
 
 /*
@@ -184,6 +190,26 @@ int umap_layout_debug_negatives(const umap_layout *h, uint64_t seed, int32_t epo
  * wavefront kernel (default), 1 = one thread per vertex.  Both compute the
  * same result bit for bit. */
 int umap_layout_set_kernel(umap_layout *h, int32_t which);
+
+/* umap_layout_set_mode -- how later runs apply their updates (embedding-updates
+ * and reproducibility sections):
+ *   UMAP_MODE_SYNC   epoch-synchronous (default): E_{n+1} = E_n + alpha_n x
+ *                    the sum of the epoch's terms, every term computed from
+ *                    E_n; deterministic, bit-identical for both kernels.
+ *   UMAP_MODE_ASYNC  asynchronous, in place (Hogwild): one thread per sampled
+ *                    edge applies alpha_n x the clipped attraction to its
+ *                    source (a private copy) and the opposite change to its
+ *                    destination, then each negative sample's repulsion to
+ *                    the private copy in turn, and adds the source's change
+ *                    to the table; reads see whatever other threads have
+ *                    written, so the result depends on the timing of the
+ *                    GPU's threads and is not repeatable bit for bit.  Same
+ *                    schedule, negative draws, clip and step size as the
+ *                    synchronous mode; umap_layout_set_kernel does not apply.
+ *                    Needs rows of fewer than 2^24 - 8192 edges
+ *                    (UMAP_E_INVAL from the run otherwise).
+ * Any other value is UMAP_E_INVAL.  Takes effect at the next run. */
+int umap_layout_set_mode(umap_layout *h, int32_t mode);
 
 /* ---- quality ------------------------------------------------------------- */
 

@@ -11,7 +11,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libumap_layout.so")
 
-SOURCES = ["api.hip", "kernels_prep.hip", "kernels_layout.hip", "kernels_graph.hip", "kernels_probe.hip", "kernels_trust.hip", "fit_ab.cpp"]
+SOURCES = ["api.hip", "kernels_prep.hip", "kernels_layout.hip", "kernels_hogwild.hip", "kernels_graph.hip",
+           "kernels_probe.hip", "kernels_trust.hip", "fit_ab.cpp"]
 
 HIPCC_FLAGS = [
     "-O3", "--offload-arch=gfx950", "-std=c++17", "-fPIC", "-shared",

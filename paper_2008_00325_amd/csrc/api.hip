@@ -125,6 +125,7 @@ struct umap_layout {
     int32_t max_degree = 0;
     float w_max = 0;
     int kernel = 0;
+    int mode = 0;                           // 0 epoch-synchronous, 1 asynchronous in place
 
     void *arena = nullptr;
     int64_t *row_ptr = nullptr;
@@ -331,8 +332,12 @@ int run_epochs_impl(umap_layout *h, uint64_t seed, int32_t first, int32_t last, 
     // a row of about 2^24 edges) the one-thread-per-vertex kernel runs
     const bool fits = (h->n >> h->lg_phases) + 2 < ((int64_t)1 << 24) &&
                       (int64_t)h->max_degree + ul::kWaveCost < ((int64_t)1 << 24);
-    const int kernel = fits ? h->kernel : 1;
-    const bool records = kernel != 1;
+    const bool async = h->mode == 1;
+    if (async && (int64_t)h->max_degree + ul::kWaveCost >= ((int64_t)1 << 24))
+        return fail(UMAP_E_INVAL, "the asynchronous mode needs rows of fewer than %d edges",
+                    (1 << 24) - ul::kWaveCost);
+    const int kernel = async ? 2 : fits ? h->kernel : 1;
+    const bool records = kernel == 0;
     const int cur0 = h->cur;
     const size_t nd_bytes = sizeof(float) * (size_t)h->n * (size_t)h->dim;
     if (records) {
@@ -345,7 +350,7 @@ int run_epochs_impl(umap_layout *h, uint64_t seed, int32_t first, int32_t last, 
     // epochs [first, last) with one kernel; fault >= 0 injects a launch error
     auto epochs = [&](int which) -> int {
         UL_HIP(ul::launch_zero_u64(h->active, h->n_epochs, h->stream));
-        const int64_t slots = ul::count_slots(which, h->n, h->n_waves);
+        const int64_t slots = ul::count_slots(which == 1 ? 1 : 0, h->n, h->n_waves);
         const int ring = h->n_epochs < ul::kCountRing ? h->n_epochs : ul::kCountRing;
         int32_t pending_from = first;   // first epoch whose counts are not yet summed
         for (int32_t ep = first; ep < last; ++ep) {
@@ -353,13 +358,18 @@ int run_epochs_impl(umap_layout *h, uint64_t seed, int32_t first, int32_t last, 
                 UL_HIP(hipStreamSynchronize(h->stream));
                 return fail(UMAP_E_DEVICE, "epoch %d launch failed [injected]", ep);
             }
-            A.E = h->E[h->cur];
-            A.E_next = h->E[1 - h->cur];
             A.epoch = ep;
             A.alpha = 1.0 - (double)ep / (double)h->n_epochs;
             A.counts = h->counts + (int64_t)((ep - pending_from) % ring) * h->count_stride;
-            UL_HIP(ul::launch_epoch(which, h->dim, A, G, h->stream));
-            h->cur = 1 - h->cur;
+            if (which == 2) {
+                A.E = A.E_next = h->E[h->cur];   // in place
+                UL_HIP(ul::launch_epoch_hogwild(h->dim, A, G, h->stream));
+            } else {
+                A.E = h->E[h->cur];
+                A.E_next = h->E[1 - h->cur];
+                UL_HIP(ul::launch_epoch(which, h->dim, A, G, h->stream));
+                h->cur = 1 - h->cur;
+            }
             if (ep + 1 - pending_from == ring || ep + 1 == last) {
                 UL_HIP(ul::launch_reduce_counts(h->counts, h->count_stride, slots, ep + 1 - pending_from,
                                                 h->active + pending_from, h->stream));
@@ -558,6 +568,7 @@ int umap_layout_stats(const umap_layout *h, umap_layout_stats_t *out)
     s.w_max = h->w_max;
     s.table_ranges = 1 << h->lg_phases;
     s.kernel = h->kernel;
+    s.mode = h->mode;
     *out = s;
     return UMAP_OK;
 }
@@ -579,6 +590,15 @@ int umap_layout_set_kernel(umap_layout *h, int32_t which)
     if (!h) return fail(UMAP_E_INVAL, "handle is NULL");
     if (which != 0 && which != 1) return fail(UMAP_E_INVAL, "kernel must be 0 or 1, got %d", which);
     h->kernel = which;
+    return UMAP_OK;
+}
+
+int umap_layout_set_mode(umap_layout *h, int32_t mode)
+{
+    if (!h) return fail(UMAP_E_INVAL, "handle is NULL");
+    if (mode != UMAP_MODE_SYNC && mode != UMAP_MODE_ASYNC)
+        return fail(UMAP_E_INVAL, "mode must be %d or %d, got %d", UMAP_MODE_SYNC, UMAP_MODE_ASYNC, mode);
+    h->mode = mode;
     return UMAP_OK;
 }
 

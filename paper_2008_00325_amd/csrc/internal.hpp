@@ -107,6 +107,8 @@ constexpr int64_t kPhaseTableBytes = 2 << 20;
 int32_t phase_log2(int64_t n, int32_t dim);
 
 hipError_t launch_epoch(int kernel, int32_t dim, const EpochArgs &A, const WaveGraph &G, hipStream_t s);
+// One asynchronous epoch, in place on A.E_next (A.E must be the same buffer).
+hipError_t launch_epoch_hogwild(int32_t dim, const EpochArgs &A, const WaveGraph &G, hipStream_t s);
 // Count slots one epoch of `kernel` writes (one per wave).
 int64_t count_slots(int kernel, int64_t n, int64_t n_waves);
 // out[r] = sum of counts[r * stride + 0 .. slots) for r < rows.

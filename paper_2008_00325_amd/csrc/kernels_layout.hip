@@ -115,15 +115,10 @@ __global__ __launch_bounds__(256) void k_epoch_rowwise(EpochArgs A, const int64_
 //    vertex table, which is sized to stay resident in an XCD's L2.  The last
 //    range commits the wave's rows of E_{n+1} with coalesced stores.
 // ---------------------------------------------------------------------------
-constexpr int kWavesPerBlock = 4;
 // The eps / col / head stream is read in super-chunks of kSuper x 64 edges,
 // double buffered in registers: super-chunk s+1 is in flight while s is
 // classified.
 constexpr int kSuper = 2;
-// Rows staged in LDS on each side of a wave's own rows: the attraction reads
-// y_j from there when j is that close (neighbour lists of locally ordered
-// vertices), and from global memory otherwise.
-constexpr int kHalo = 64;
 // Records per lane per step of the repulsion kernel.
 constexpr int kRepUnroll = 16;
 // LDS ring of sampled edges waiting for their attraction and draws: (tail,
@@ -131,24 +126,6 @@ constexpr int kRepUnroll = 16;
 // one super-chunk.
 constexpr int kQueue = 256;
 static_assert(kQueue >= kWave - 1 + kSuper * kWave, "queue too small");
-
-__device__ __forceinline__ int64_t uniform64(int64_t v)
-{
-    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)(uint64_t)v);
-    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)v >> 32));
-    return (int64_t)(((uint64_t)hi << 32) | lo);
-}
-
-// Logical wave index of this lane's wave.  Workgroups are dispatched
-// round-robin over the 8 XCDs; each XCD gets a contiguous run of logical
-// blocks so that neighbouring rows (and their mostly-local neighbours) share
-// one L2.
-__device__ __forceinline__ int64_t logical_wave()
-{
-    const int64_t per_xcd = gridDim.x / 8;
-    const int64_t lb = (int64_t)(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
-    return lb * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-}
 
 // first vertex of table range p of P = 2^lg (ranges split the 32-bit draw)
 __device__ __forceinline__ uint32_t range_base(uint32_t p, int32_t lg, uint32_t n)

@@ -197,6 +197,31 @@ __device__ __forceinline__ void wave_sync()
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Wavefronts per workgroup of the edge-parallel kernels.
+constexpr int kWavesPerBlock = 4;
+// Rows staged in LDS on each side of a wave's own rows: the attraction reads
+// y_j from there when j is that close (neighbour lists of locally ordered
+// vertices), and from global memory otherwise.
+constexpr int kHalo = 64;
+
+__device__ __forceinline__ int64_t uniform64(int64_t v)
+{
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)(uint64_t)v);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)v >> 32));
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+// Logical wave index of this lane's wave in a grid of a multiple of 8
+// workgroups.  Workgroups are dispatched round-robin over the 8 XCDs; each XCD
+// gets a contiguous run of logical blocks so that neighbouring rows (and their
+// mostly-local neighbours) share one L2.
+__device__ __forceinline__ int64_t logical_wave()
+{
+    const int64_t per_xcd = gridDim.x / 8;
+    const int64_t lb = (int64_t)(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+    return lb * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+}
+
 __device__ __forceinline__ unsigned lane_id() { return __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u)); }
 
 // Number of set bits of `mask` below the calling lane.

@@ -24,12 +24,14 @@ UMAP_E_ASYMMETRIC = -2
 UMAP_E_NOMEM = -3
 UMAP_E_DEVICE = -4
 UMAP_E_STATE = -5
+UMAP_MODE_SYNC = 0
+UMAP_MODE_ASYNC = 1
 
 EXPORTS = (
     "umap_layout_create", "umap_layout_create_device", "umap_layout_run", "umap_layout_run_epochs",
     "umap_layout_get", "umap_layout_get_device", "umap_layout_set_embedding", "umap_layout_get_graph",
     "umap_layout_stats", "umap_layout_set_stream", "umap_layout_destroy", "umap_layout_last_error",
-    "umap_layout_debug_active", "umap_layout_debug_negatives", "umap_layout_set_kernel",
+    "umap_layout_debug_active", "umap_layout_debug_negatives", "umap_layout_set_kernel", "umap_layout_set_mode",
     "umap_fuzzy_graph_device", "umap_fit_ab", "umap_probe_copy", "umap_probe_gather",
     "umap_trustworthiness",
 )
@@ -54,6 +56,7 @@ class umap_layout_stats_t(ctypes.Structure):
         ("table_ranges", ctypes.c_int32),
         ("kernel", ctypes.c_int32),
         ("overflow_redone", ctypes.c_int32),
+        ("mode", ctypes.c_int32),
     ]
 
     def as_dict(self) -> dict:
@@ -94,6 +97,7 @@ def lib() -> ctypes.CDLL:
             "umap_layout_debug_active": [P, i32, P],
             "umap_layout_debug_negatives": [P, u64, i32, i64, i64, P],
             "umap_layout_set_kernel": [P, i32],
+            "umap_layout_set_mode": [P, i32],
             "umap_fuzzy_graph_device": [i64, i32, P, P, P, P, P, P],
             "umap_fit_ab": [f32, f32, ctypes.POINTER(f32), ctypes.POINTER(f32)],
             "umap_probe_copy": [P, P, i64, P],
@@ -240,6 +244,10 @@ def umap_layout_set_stream(h: Handle, stream) -> None:
 
 def umap_layout_set_kernel(h: Handle, which: int) -> None:
     _check(lib().umap_layout_set_kernel(h.ptr, which))
+
+
+def umap_layout_set_mode(h: Handle, mode: int) -> None:
+    _check(lib().umap_layout_set_mode(h.ptr, mode))
 
 
 def umap_layout_destroy(h: Handle) -> None:

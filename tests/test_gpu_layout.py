@@ -348,6 +348,41 @@ def test_full_run_trustworthiness(blobs_graph):
         assert np.all(np.isfinite(Eg))
 
 
+@pytest.mark.parametrize("dim,R", [(2, 5), (3, 5), (16, 10), (2, 0)])
+def test_async_mode_quality(dim, R, blobs_graph):
+    """Asynchronous (Hogwild) mode, the paper's default: not repeatable bit for
+    bit, so the check is on quality -- T@15 of a full run within 0.01 of the
+    oracle's (epoch-synchronous) run at the same settings -- plus the parts that
+    stay deterministic (the number of sampled edges, the mode switch)."""
+    w, X, ids, dist, (r, c, v) = blobs_graph
+    g = O.prep(w.n, r, c, v, w.n_epochs)
+    a, b = O.fit_ab(w.spread, w.min_dist)
+    seed = 4
+    case(f"async blobs2k dim {dim} R {R}")
+    with U.umap_layout_create(w.n, dim, r, c, v, a, b, w.n_epochs, R) as h:
+        U.umap_layout_run(h, seed)
+        Es = U.umap_layout_get(h)
+        U.umap_layout_set_mode(h, U.UMAP_MODE_ASYNC)
+        U.umap_layout_run(h, seed)
+        Ea = U.umap_layout_get(h)
+        st = U.umap_layout_stats(h)
+        assert st["mode"] == U.UMAP_MODE_ASYNC
+        with pytest.raises(U.UmapLayoutError) as ei:
+            U.umap_layout_set_mode(h, 2)
+        assert ei.value.code == U.UMAP_E_INVAL
+        U.umap_layout_set_mode(h, U.UMAP_MODE_SYNC)
+        U.umap_layout_run(h, seed)
+        assert np.array_equal(U.umap_layout_get(h).view(np.uint32), Es.view(np.uint32))
+    Eo, act = O.run(g, dim, a, b, w.n_epochs, R, seed)
+    assert st["active_edges"] == int(act.sum())
+    assert st["edge_updates"] == int(act.sum()) * (1 + R)
+    assert np.all(np.isfinite(Ea))
+    ta = O.trustworthiness(X, Ea, 15)
+    to = O.trustworthiness(X, Eo, 15)
+    print(f"  T(async) = {ta:.5f}  T(oracle) = {to:.5f}", flush=True)
+    assert abs(ta - to) <= 0.01
+
+
 def test_fault_injection(monkeypatch, blobs_graph):
     w, X, ids, dist, (r, c, v) = blobs_graph
     case("fault injection")
@@ -548,19 +583,25 @@ def test_full_run_trustworthiness_image70k():
     a, b = O.fit_ab(w.spread, w.min_dist)
     g = O.prep(w.n, r, c, v, w.n_epochs)
     seed = 3
-    case("image70k: GPU layout")
+    case("image70k: GPU layouts (synchronous, asynchronous)")
     with U.umap_layout_create(w.n, w.dim, r, c, v, a, b, w.n_epochs, w.neg_rate) as h:
         _check_graph(h, g)
         U.umap_layout_run(h, seed)
         Eg = U.umap_layout_get(h)
         st = U.umap_layout_stats(h)
+        U.umap_layout_set_mode(h, U.UMAP_MODE_ASYNC)
+        U.umap_layout_run(h, seed)
+        Ea = U.umap_layout_get(h)
+        sta = U.umap_layout_stats(h)
     case("image70k: oracle layout")
     Eo, act = O.run(g, w.dim, a, b, w.n_epochs, w.neg_rate, seed)
-    assert st["active_edges"] == int(act.sum())
-    assert np.all(np.isfinite(Eg))
-    case("image70k: trustworthiness of both")
+    assert st["active_edges"] == int(act.sum()) == sta["active_edges"]
+    assert np.all(np.isfinite(Eg)) and np.all(np.isfinite(Ea))
+    case("image70k: trustworthiness of the three layouts")
     Xg = torch.from_numpy(X).cuda()
     tg = U.umap_trustworthiness(Xg, torch.from_numpy(Eg).cuda(), 15)
+    ta = U.umap_trustworthiness(Xg, torch.from_numpy(Ea).cuda(), 15)
     to = U.umap_trustworthiness(Xg, torch.from_numpy(Eo.astype(np.float32)).cuda(), 15)
-    print(f"  T@15(gpu layout) = {tg:.5f}  T@15(oracle layout) = {to:.5f}", flush=True)
+    print(f"  T@15(gpu) = {tg:.5f}  T@15(gpu async) = {ta:.5f}  T@15(oracle) = {to:.5f}", flush=True)
     assert abs(tg - to) <= 0.01
+    assert abs(ta - to) <= 0.01
