@@ -128,6 +128,16 @@ int umap_layout_create_device(umap_layout **out, int64_t n, int32_t n_components
 int umap_layout_run(umap_layout *h, uint64_t seed);
 
 /*
+ * umap_layout_init -- only the initialisation of umap_layout_run: the uniform
+ * random layout on [-10, 10) from `seed` for a fit (embedding-updates section),
+ * the weighted mean of the kept neighbours for a transform.  Afterwards
+ * umap_layout_run_epochs(h, seed, 0, N) equals umap_layout_run(h, seed), and
+ * the epochs can be taken in pieces (e.g. to look at the layout in between).
+ * Blocking.
+ */
+int umap_layout_init(umap_layout *h, uint64_t seed);
+
+/*
  * umap_layout_run_epochs -- epochs first .. last-1 (0 <= first <= last <= N)
  * from the current layout, without initialisation.  Because the random
  * streams are counter-based, running 0..m then m..N equals one run of 0..N.
@@ -171,6 +181,43 @@ void umap_layout_destroy(umap_layout *h);
 /* umap_layout_last_error -- message of the last failing call on this thread
  * ("" if none).  Valid until the next failing call on this thread. */
 const char *umap_layout_last_error(void);
+
+/*
+ * umap_transform_create -- a handle that lays out n_new new points against a
+ * frozen trained layout (inference: the model section keeps the training kNN
+ * index to map new points; the embedding-updates section moves only the new
+ * points).  The graph is bipartite: row i is new point i, column j is row j of
+ * the table, with weight v (e.g. the membership strength of Eq. 1 of the new
+ * point's kNN among the training points; no union, no symmetry).
+ *
+ *   out        receives the handle (NULL on failure).
+ *   n_new      new points, 1 <= n_new < 2^31.
+ *   n_components  embedding dimension, 1..16 (the table's).
+ *   table      n_table x n_components fp32 trained layout, row-major, host
+ *              memory (read only; copied, the caller keeps ownership).
+ *   n_table    rows of the table, 1 <= n_table < 2^31.
+ *   rows, cols nnz int32 indices, rows in [0, n_new), cols in [0, n_table)
+ *              (host memory, read only).  Equal row and column indices are
+ *              ordinary edges here.
+ *   vals       nnz fp32 weights, finite; entries <= 0 are dropped, the rest
+ *              pruned below w_max / n_epochs as in a fit.
+ *   a, b, n_epochs, neg_rate  as for umap_layout_create (negative samples are
+ *              drawn from the table's rows).
+ *
+ * The handle takes the same calls as a fit's, with these differences:
+ * umap_layout_run initialises every new point at the mean of its kept
+ * neighbours' table rows weighted by 1/eps_e (the origin when it has none) --
+ * the seed then only keys the negative samples -- and each sampled edge (i, j)
+ * moves new point i by alpha_n x the clipped attraction toward table row j
+ * (once: the table does not move and there is no reverse edge), each negative
+ * sample k by alpha_n x the clipped repulsion from table row k.  Updates are
+ * epoch-synchronous and deterministic; UMAP_MODE_ASYNC is not available
+ * (UMAP_E_INVAL from the run).  Errors: UMAP_E_INVAL for bad arguments or
+ * indices, UMAP_E_NOMEM, UMAP_E_DEVICE; never UMAP_E_ASYMMETRIC.
+ */
+int umap_transform_create(umap_layout **out, int64_t n_new, int32_t n_components, const float *table,
+                          int64_t n_table, const int32_t *rows, const int32_t *cols, const float *vals, int64_t nnz,
+                          float a, float b, int32_t n_epochs, int32_t neg_rate);
 
 /* ---- diagnostics (tests, measurement) ---------------------------------- */
 

@@ -337,3 +337,175 @@ def trustworthiness(X: np.ndarray, Y: np.ndarray, k: int = 15, rows: np.ndarray 
             total += float(np.maximum(rk - k, 0).sum())
     total *= n / rows.size
     return 1.0 - 2.0 / (n * k * (2.0 * n - 3.0 * k - 1.0)) * total
+
+
+# --------------------------------------------------------------------------
+# Quality of graph-only workloads (no input coordinates, so no
+# trustworthiness): neighbour recall and the objective of the UMAP section on
+# a seeded vertex sample.
+# --------------------------------------------------------------------------
+
+def recall_at_k(knn_ids: np.ndarray, Y: np.ndarray, rows: np.ndarray, k: int = 15) -> float:
+    """Mean over `rows` of |N_in(i) & N_emb(i)| / k, N_in(i) the first k
+    entries of i's input neighbour list (nearest first), N_emb(i) the k
+    nearest other vertices of i in the layout Y (Euclidean in fp64; a k-d tree
+    finds them, ties in any order).  Pinned: 1 for the exact kNN of Y itself;
+    hand-checked counts on a small line layout."""
+    from scipy.spatial import cKDTree
+
+    Y64 = np.asarray(Y, dtype=np.float64)
+    rows = np.asarray(rows, dtype=np.int64)
+    _, nb = cKDTree(Y64).query(Y64[rows], k=k + 1)
+    hits = 0
+    for t, i in enumerate(rows):
+        emb = [int(j) for j in nb[t] if j != i][:k]
+        hits += len(set(emb) & set(int(j) for j in knn_ids[i, :k]))
+    return hits / (k * rows.size)
+
+
+def objective(g: Graph, Y: np.ndarray, a: float, b: float, neg_rate: int, rows: np.ndarray,
+              negatives: np.ndarray) -> float:
+    """The cross-entropy objective of the UMAP section, restricted to the edges
+    of the sampled vertices `rows`:
+        sum_i sum_{e = (i, j)} f_e ( -log Phi(y_i, y_j)
+                                      - neg_rate * mean_c log(1 - Phi(y_i, y_c)) ),
+    Phi(x, y) = 1 / (1 + a |x - y|^(2b)), f_e = 1 / eps_e the fraction of epochs
+    in which e is sampled, c over the fixed vertices negatives[t] of the t-th
+    row (c = i skipped).  log(1 - Phi) is taken as log(a d^(2b) / (1 + a d^(2b)))
+    with d^2 floored at 1e-12 (coincident points).  Pinned: closed-form values
+    on two points; its derivative matches the gradient coefficients."""
+    Y64 = np.asarray(Y, dtype=np.float64)
+    rows = np.asarray(rows, dtype=np.int64)
+    total = 0.0
+    for t, i in enumerate(rows):
+        lo, hi = int(g.row_ptr[i]), int(g.row_ptr[i + 1])
+        if hi == lo:
+            continue
+        f = 1.0 / g.eps[lo:hi].astype(np.float64)
+        d2 = ((Y64[g.col[lo:hi]] - Y64[i]) ** 2).sum(1)
+        attract = np.log1p(a * d2 ** b)                       # -log Phi
+        c = negatives[t][negatives[t] != i]
+        dc2 = np.maximum(((Y64[c] - Y64[i]) ** 2).sum(1), 1e-12)
+        p = a * dc2 ** b
+        repel = -(np.log(p) - np.log1p(p)).mean() if c.size else 0.0   # -log(1 - Phi)
+        total += float((f * (attract + neg_rate * repel)).sum())
+    return total
+
+
+# --------------------------------------------------------------------------
+# Transform (inference): new points laid out against a frozen trained layout;
+# only the new points move (embedding-updates section; model section on the
+# kept kNN index).  Plain numpy, fp64 state, the fp32 schedule of `prep`.
+# --------------------------------------------------------------------------
+
+def prep_bipartite(n: int, n_table: int, rows, cols, vals, n_epochs: int) -> Graph:
+    """Drop/prune/sort/eps of the graph from n new points (rows) to the n_table
+    vertices of a frozen layout (columns): the steps of `prep` without the
+    self-loop drop (a row and a column with the same index are different
+    vertices) and without the symmetry requirement."""
+    rows = np.asarray(rows, dtype=np.int64)
+    cols = np.asarray(cols, dtype=np.int64)
+    vals = np.asarray(vals, dtype=np.float32)
+    if rows.size and (rows.min() < 0 or rows.max() >= n or cols.min() < 0 or cols.max() >= n_table):
+        raise PrepError(-1)
+    if not np.all(np.isfinite(vals)):
+        raise PrepError(-1)
+    cand = vals > 0
+    w_max = np.float32(vals[cand].max()) if cand.any() else np.float32(0)
+    keep = cand & (vals >= w_max / np.float32(n_epochs))
+    r, c, v = rows[keep], cols[keep], vals[keep]
+    order = np.lexsort((c, r))
+    r, c, v = r[order], c[order], v[order]
+    if r.size > 1 and np.any((r[1:] == r[:-1]) & (c[1:] == c[:-1])):
+        raise PrepError(-1)
+    row_ptr = np.zeros(n + 1, dtype=np.int64)
+    row_ptr[1:] = np.cumsum(np.bincount(r, minlength=n))
+    eps = (w_max / v).astype(np.float32)
+    return Graph(n, row_ptr, c.astype(np.int32), eps, float(w_max))
+
+
+def transform_init(g: Graph, T: np.ndarray) -> np.ndarray:
+    """Initial position of each new point: the mean of its kept neighbours'
+    positions in the frozen layout T, weighted by 1/eps_e (the edge weight over
+    w_max); a point without kept edges starts at the origin."""
+    T64 = np.asarray(T, dtype=np.float64)
+    w = 1.0 / g.eps.astype(np.float64)
+    heads = g.heads()
+    num = np.zeros((g.n, T64.shape[1]))
+    den = np.zeros(g.n)
+    np.add.at(num, heads, w[:, None] * T64[g.col])
+    np.add.at(den, heads, w)
+    Y = np.zeros_like(num)
+    has = den > 0
+    Y[has] = num[has] / den[has, None]
+    return Y
+
+
+def _attr_coef_v(d2: np.ndarray, a: float, b: float) -> np.ndarray:
+    """d/dy_i log Phi = c (y_i - y_j), c = -2ab d2^(b-1) / (1 + a d2^b); 0 at d2 = 0."""
+    safe = np.where(d2 > 0, d2, 1.0)
+    return np.where(d2 > 0, -2.0 * a * b * safe ** (b - 1.0) / (1.0 + a * safe ** b), 0.0)
+
+
+def _rep_coef_v(d2: np.ndarray, a: float, b: float) -> np.ndarray:
+    """d/dy_i log(1 - Phi), regularised: c = 2b / ((1e-3 + d2)(1 + a d2^b)); 0 at d2 = 0."""
+    safe = np.where(d2 > 0, d2, 1.0)
+    return np.where(d2 > 0, 2.0 * b / ((1e-3 + safe) * (1.0 + a * safe ** b)), 0.0)
+
+
+def frozen_epoch(g: Graph, E: np.ndarray, T: np.ndarray, epoch_idx: int, a: float, b: float, n_epochs: int,
+                 neg_rate: int, seed: int, attr_mult: float = 1.0, self_skip: bool = False):
+    """One epoch-synchronous step in which only the rows of g move (pull form,
+    fp64): for every sampled edge e = (i, j), y_i gains alpha * attr_mult *
+    clip(attraction toward T_j), and for each of its neg_rate draws k from
+    [0, n_table) alpha * clip(repulsion from T_k).  A transform uses
+    attr_mult = 1 and T the frozen layout; with T = E, attr_mult = 2 and draws
+    equal to the source skipped this is the fit's epoch (each row also takes
+    the equal share of its reverse edge).  Returns (E', sampled edges)."""
+    E64 = np.asarray(E, dtype=np.float64)
+    T64 = np.asarray(T, dtype=np.float64)
+    alpha = 1.0 - epoch_idx / n_epochs
+    e_act = np.nonzero(active_mask(g.eps, epoch_idx))[0]
+    i = g.heads()[e_act].astype(np.int64)
+    j = g.col[e_act].astype(np.int64)
+    delta = np.zeros_like(E64)
+    diff = E64[i] - T64[j]
+    d2 = (diff * diff).sum(1)
+    np.add.at(delta, i, alpha * attr_mult * np.clip(_attr_coef_v(d2, a, b)[:, None] * diff, -4.0, 4.0))
+    if neg_rate > 0 and e_act.size:
+        ks = negative_vertices(seed, epoch_idx, 0, g.nnz, neg_rate, T64.shape[0])[e_act].astype(np.int64)
+        for r in range(neg_rate):
+            k = ks[:, r]
+            sel = k != i if self_skip else np.ones(k.size, dtype=bool)
+            diff = E64[i[sel]] - T64[k[sel]]
+            d2 = (diff * diff).sum(1)
+            np.add.at(delta, i[sel], alpha * np.clip(_rep_coef_v(d2, a, b)[:, None] * diff, -4.0, 4.0))
+    return E64 + delta, int(e_act.size)
+
+
+def transform_run(g: Graph, T: np.ndarray, a: float, b: float, n_epochs: int, neg_rate: int, seed: int):
+    """transform_init, then n_epochs frozen epochs.  Returns (Y_N, sampled edges per epoch)."""
+    Y = transform_init(g, T)
+    act = np.empty(n_epochs, dtype=np.int64)
+    for ep in range(n_epochs):
+        Y, act[ep] = frozen_epoch(g, Y, T, ep, a, b, n_epochs, neg_rate, seed)
+    return Y, act
+
+
+def exact_knn_cross(Q: np.ndarray, X: np.ndarray, k: int, batch: int = 1024) -> tuple[np.ndarray, np.ndarray]:
+    """k nearest rows of X for every row of Q (Euclidean, fp64, ties by smaller
+    index): the kNN query of new points against the kept training index."""
+    Q64 = Q.astype(np.float64)
+    X64 = X.astype(np.float64)
+    ids = np.empty((Q.shape[0], k), dtype=np.int32)
+    dist = np.empty((Q.shape[0], k), dtype=np.float32)
+    for s in range(0, Q.shape[0], batch):
+        t = min(Q.shape[0], s + batch)
+        D = _sqdist(Q64[s:t], X64)
+        cand = np.argpartition(D, k, axis=1)[:, : k + 1]
+        diff = Q64[s:t, None, :] - X64[cand]
+        ed = np.sqrt((diff * diff).sum(-1))
+        order = np.lexsort((cand, ed), axis=1)[:, :k]
+        ids[s:t] = np.take_along_axis(cand, order, axis=1)
+        dist[s:t] = np.take_along_axis(ed, order, axis=1)
+    return ids, dist

@@ -126,6 +126,8 @@ struct umap_layout {
     float w_max = 0;
     int kernel = 0;
     int mode = 0;                           // 0 epoch-synchronous, 1 asynchronous in place
+    float *table = nullptr;                 // transform: the frozen layout (n_table x dim), else null
+    int64_t n_table = 0;                    // rows of the table the tails and negatives index
 
     void *arena = nullptr;
     int64_t *row_ptr = nullptr;
@@ -161,9 +163,12 @@ struct umap_layout {
 
 namespace {
 
+// A fit (table == nullptr: B is symmetric over n vertices) or a transform
+// (rows are n new points, columns index the n_table rows of the frozen host
+// layout `table`).
 int create_common(umap_layout **out, int64_t n, int32_t dim, const int32_t *rows, const int32_t *cols,
                   const float *vals, int64_t nnz, float a, float b, int32_t n_epochs, int32_t neg_rate,
-                  hipStream_t stream, bool host_inputs)
+                  hipStream_t stream, bool host_inputs, const float *table = nullptr, int64_t n_table = 0)
 {
     umap_layout *h = new (std::nothrow) umap_layout();
     if (!h) return fail(UMAP_E_NOMEM, "host allocation failed");
@@ -183,6 +188,7 @@ int create_common(umap_layout **out, int64_t n, int32_t dim, const int32_t *rows
         h->n_epochs = n_epochs;
         h->neg_rate = neg_rate;
         h->nnz_in = nnz;
+        h->n_table = table ? n_table : n;
         for (auto &e : h->ev) UL_HIP(hipEventCreate(&e));
 
         // persistent arena; the wave count is bounded with nnz (kept <= nnz)
@@ -192,14 +198,15 @@ int create_common(umap_layout **out, int64_t n, int32_t dim, const int32_t *rows
         const int64_t count_stride =
             ul::count_slots(1, n, 0) > max_waves ? ul::count_slots(1, n, 0) : max_waves;
         const int64_t count_rows = n_epochs < ul::kCountRing ? n_epochs : ul::kCountRing;
-        const int32_t lg_phases = ul::phase_log2(n, dim);
+        const int32_t lg_phases = ul::phase_log2(h->n_table, dim);
+        const size_t table_elems = table ? (size_t)n_table * (size_t)dim : 0;
         const int64_t n_phases = (int64_t)1 << lg_phases;
         size_t bytes = need<int64_t>(n + 1) + need<int32_t>(nnz) + need<float>(nnz) + need<int32_t>(max_waves + 1) +
                        2 * need<float>(nd) + need<unsigned long long>(n_epochs) + need<uint8_t>(nnz) +
                        need<int32_t>((size_t)count_rows * count_stride) +
                        need<uint32_t>(ul::record_offset(max_waves, nnz, neg_rate, (int32_t)n_phases)) +
                        need<int32_t>((size_t)n_phases * max_waves) + need<long long>(nd) + need<unsigned>(1) +
-                       need<float>(nd);
+                       need<float>(nd) + need<float>(table_elems);
         if (fault_alloc()) throw HipFailure{hipErrorOutOfMemory, "hipMalloc(arena) [injected]"};
         UL_HIP(hipMalloc(&h->arena, bytes));
         Carver cv{static_cast<char *>(h->arena)};
@@ -219,11 +226,17 @@ int create_common(umap_layout **out, int64_t n, int32_t dim, const int32_t *rows
         h->delta = cv.take<long long>(nd);
         h->overflow = cv.take<unsigned>(1);
         h->E_start = cv.take<float>(nd);
+        if (table) {
+            h->table = cv.take<float>(table_elems);
+            UL_HIP(hipMemcpyAsync(h->table, table, sizeof(float) * table_elems, hipMemcpyHostToDevice, stream));
+        }
 
         // ingest scratch (stream-ordered)
         ul::PrepBuffers B{};
         B.nnz = nnz;
         B.n = n;
+        B.n_cols = h->n_table;
+        B.bipartite = table != nullptr;
         B.n_epochs = n_epochs;
         B.nblocks_scan = ul::scan_blocks(n);
         size_t sbytes = 2 * need<int32_t>(n) + 2 * need<int32_t>(nnz) + 2 * need<float>(nnz) +
@@ -275,7 +288,9 @@ int create_common(umap_layout **out, int64_t n, int32_t dim, const int32_t *rows
         scratch = nullptr;
 
         int rc = UMAP_OK;
-        if (S.flags & ul::kBadIndex) rc = fail(UMAP_E_INVAL, "a row or column index is outside [0, n)");
+        if (S.flags & ul::kBadIndex)
+            rc = table ? fail(UMAP_E_INVAL, "a row index is outside [0, n_new) or a column outside [0, n_table)")
+                       : fail(UMAP_E_INVAL, "a row or column index is outside [0, n)");
         else if (S.flags & ul::kBadValue) rc = fail(UMAP_E_INVAL, "a value is not finite");
         else if (S.flags & ul::kDuplicate) rc = fail(UMAP_E_INVAL, "an edge (i, j) is listed more than once");
         else if (S.flags & ul::kAsymmetric)
@@ -317,6 +332,9 @@ int run_epochs_impl(umap_layout *h, uint64_t seed, int32_t first, int32_t last, 
     const int fault = fault_launch_epoch();
     ul::EpochArgs A{};
     A.n = (uint32_t)h->n;
+    A.n_table = (uint32_t)h->n_table;
+    A.same_table = h->table ? 0 : 1;
+    A.attr_mult = h->table ? 1.0f : 2.0f;
     A.neg_rate = h->neg_rate;
     A.a = h->a;
     A.b = h->b;
@@ -330,9 +348,10 @@ int run_epochs_impl(umap_layout *h, uint64_t seed, int32_t first, int32_t last, 
     // sampled edge's offset inside its wave in 24 bits (a wave holds fewer
     // than kWaveCost + max_degree edges); beyond that (n >= 2^28 vertices, or
     // a row of about 2^24 edges) the one-thread-per-vertex kernel runs
-    const bool fits = (h->n >> h->lg_phases) + 2 < ((int64_t)1 << 24) &&
+    const bool fits = (h->n_table >> h->lg_phases) + 2 < ((int64_t)1 << 24) &&
                       (int64_t)h->max_degree + ul::kWaveCost < ((int64_t)1 << 24);
     const bool async = h->mode == 1;
+    if (async && h->table) return fail(UMAP_E_INVAL, "the asynchronous mode applies to fits, not to transforms");
     if (async && (int64_t)h->max_degree + ul::kWaveCost >= ((int64_t)1 << 24))
         return fail(UMAP_E_INVAL, "the asynchronous mode needs rows of fewer than %d edges",
                     (1 << 24) - ul::kWaveCost);
@@ -363,10 +382,12 @@ int run_epochs_impl(umap_layout *h, uint64_t seed, int32_t first, int32_t last, 
             A.counts = h->counts + (int64_t)((ep - pending_from) % ring) * h->count_stride;
             if (which == 2) {
                 A.E = A.E_next = h->E[h->cur];   // in place
+                A.T = A.E;
                 UL_HIP(ul::launch_epoch_hogwild(h->dim, A, G, h->stream));
             } else {
                 A.E = h->E[h->cur];
                 A.E_next = h->E[1 - h->cur];
+                A.T = h->table ? h->table : A.E;
                 UL_HIP(ul::launch_epoch(which, h->dim, A, G, h->stream));
                 h->cur = 1 - h->cur;
             }
@@ -444,6 +465,35 @@ int umap_layout_create(umap_layout **out, int64_t n, int32_t n_components, const
     }
 }
 
+int umap_transform_create(umap_layout **out, int64_t n_new, int32_t n_components, const float *table,
+                          int64_t n_table, const int32_t *rows, const int32_t *cols, const float *vals, int64_t nnz,
+                          float a, float b, int32_t n_epochs, int32_t neg_rate)
+{
+    try {
+        if (!out) return fail(UMAP_E_INVAL, "out is NULL");
+        *out = nullptr;
+        int rc = check_scalars(n_new, n_components, nnz, a, b, n_epochs, neg_rate);
+        if (rc) return rc;
+        if (n_table < 1 || n_table >= ((int64_t)1 << 31))
+            return fail(UMAP_E_INVAL, "n_table must be in [1, 2^31), got %lld", (long long)n_table);
+        if (!table) return fail(UMAP_E_INVAL, "table is NULL");
+        if (nnz > 0 && (!rows || !cols || !vals)) return fail(UMAP_E_INVAL, "rows, cols and vals must not be NULL");
+        const size_t table_elems = (size_t)n_table * (size_t)n_components;
+        for (size_t t = 0; t < table_elems; ++t)
+            if (!isfinite(table[t])) return fail(UMAP_E_INVAL, "table entry %zu is not finite", t);
+        for (int64_t t = 0; t < nnz; ++t) {
+            if (rows[t] < 0 || rows[t] >= n_new || cols[t] < 0 || cols[t] >= n_table)
+                return fail(UMAP_E_INVAL, "entry %lld: index (%d, %d) outside [0, %lld) x [0, %lld)", (long long)t,
+                            rows[t], cols[t], (long long)n_new, (long long)n_table);
+            if (!isfinite(vals[t])) return fail(UMAP_E_INVAL, "entry %lld: value is not finite", (long long)t);
+        }
+        return create_common(out, n_new, n_components, rows, cols, vals, nnz, a, b, n_epochs, neg_rate, nullptr,
+                             true, table, n_table);
+    } catch (...) {
+        return fail(UMAP_E_NOMEM, "unexpected host failure");
+    }
+}
+
 int umap_layout_create_device(umap_layout **out, int64_t n, int32_t n_components, const int32_t *rows,
                               const int32_t *cols, const float *vals, int64_t nnz, float a, float b, int32_t n_epochs,
                               int32_t neg_rate, void *stream)
@@ -461,14 +511,42 @@ int umap_layout_create_device(umap_layout **out, int64_t n, int32_t n_components
     }
 }
 
+namespace {
+
+void init_layout(umap_layout *h, uint64_t seed)
+{
+    if (h->table)
+        UL_HIP(ul::launch_init_transform(h->row_ptr, h->col, h->eps, h->table, h->n, h->dim, h->E[h->cur],
+                                         h->stream));
+    else
+        UL_HIP(ul::launch_init(h->E[h->cur], h->n, h->dim, seed, h->stream));
+    h->has_layout = true;
+}
+
+}  // namespace
+
+int umap_layout_init(umap_layout *h, uint64_t seed)
+{
+    if (!h) return fail(UMAP_E_INVAL, "handle is NULL");
+    try {
+        UL_HIP(hipSetDevice(h->device));
+        init_layout(h, seed);
+        UL_HIP(hipStreamSynchronize(h->stream));
+        return UMAP_OK;
+    } catch (const HipFailure &f) {
+        return hip_fail(f);
+    } catch (...) {
+        return fail(UMAP_E_NOMEM, "unexpected host failure");
+    }
+}
+
 int umap_layout_run(umap_layout *h, uint64_t seed)
 {
     if (!h) return fail(UMAP_E_INVAL, "handle is NULL");
     try {
         UL_HIP(hipSetDevice(h->device));
         UL_HIP(hipEventRecord(h->ev[0], h->stream));
-        UL_HIP(ul::launch_init(h->E[h->cur], h->n, h->dim, seed, h->stream));
-        h->has_layout = true;
+        init_layout(h, seed);
         return run_epochs_impl(h, seed, 0, h->n_epochs, true);
     } catch (const HipFailure &f) {
         return hip_fail(f);
@@ -644,7 +722,7 @@ int umap_layout_debug_negatives(const umap_layout *h, uint64_t seed, int32_t epo
     try {
         UL_HIP(hipSetDevice(h->device));
         UL_HIP(hipMallocAsync((void **)&d, bytes, h->stream));
-        UL_HIP(ul::launch_debug_negatives((uint32_t)h->n, seed, epoch, e_first, count, h->neg_rate, d, h->stream));
+        UL_HIP(ul::launch_debug_negatives((uint32_t)h->n_table, seed, epoch, e_first, count, h->neg_rate, d, h->stream));
         UL_HIP(hipMemcpyAsync(out, d, bytes, hipMemcpyDeviceToHost, h->stream));
         UL_HIP(hipFreeAsync(d, h->stream));
         d = nullptr;

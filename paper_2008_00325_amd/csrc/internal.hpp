@@ -43,7 +43,9 @@ struct PrepBuffers {
     const int32_t *cols;
     const float *vals;
     int64_t nnz;
-    int64_t n;
+    int64_t n;          // rows
+    int64_t n_cols;     // columns are in [0, n_cols); n unless bipartite
+    bool bipartite;     // rows and columns are different vertex sets (no self loops, no symmetry)
     int32_t n_epochs;
     // scratch (device, capacity nnz or n)
     int32_t *deg;       // n
@@ -69,6 +71,8 @@ hipError_t launch_zero_u64(unsigned long long *p, int64_t count, hipStream_t s);
 
 // ---- layout (kernels_layout.hip) ----
 hipError_t launch_init(float *E, int64_t n, int32_t dim, uint64_t seed, hipStream_t s);
+hipError_t launch_init_transform(const int64_t *row_ptr, const int32_t *col, const float *eps, const float *T,
+                                 int64_t n, int32_t dim, float *E, hipStream_t s);
 // Graph-side arrays of the epoch kernels.
 struct WaveGraph {
     const int64_t *row_ptr;   // n + 1

@@ -5,6 +5,8 @@
 // snapshot E_n, every term is converted to fixed point on its own and summed in
 // int64, and E_{n+1} = E_n + alpha * sum is written to the other buffer (no
 // scatter to global memory, no atomics on the embedding in global memory).
+// In a transform the tails and negative samples are rows of a frozen layout T
+// (the trained embedding) and only the new points, the rows of E, move.
 //  * edge-parallel (default): one k_epoch_draw launch and P k_epoch_repulse
 //    launches per epoch, each wavefront owning a range of whole rows (see the
 //    section comment below).
@@ -50,6 +52,37 @@ hipError_t launch_init(float *E, int64_t n, int32_t dim, uint64_t seed, hipStrea
     return hipGetLastError();
 }
 
+// Transform: each new point starts at the mean of its kept neighbours in the
+// frozen layout T weighted by 1/eps_e (the edge weight over w_max), summed in
+// fp64 in edge order; a point without kept edges starts at the origin.
+__global__ __launch_bounds__(256) void k_init_transform(const int64_t *__restrict__ row_ptr,
+                                                        const int32_t *__restrict__ col,
+                                                        const float *__restrict__ eps, const float *__restrict__ T,
+                                                        int64_t n, int32_t dim, float *__restrict__ E)
+{
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+        const int64_t e0 = row_ptr[i], e1 = row_ptr[i + 1];
+        double den = 0.0;
+        for (int64_t e = e0; e < e1; ++e) den += 1.0 / (double)eps[e];
+        for (int32_t d = 0; d < dim; ++d) {
+            double num = 0.0;
+            for (int64_t e = e0; e < e1; ++e) num += (1.0 / (double)eps[e]) * (double)T[(size_t)col[e] * dim + d];
+            E[(size_t)i * dim + d] = den > 0.0 ? (float)(num / den) : 0.0f;
+        }
+    }
+}
+
+hipError_t launch_init_transform(const int64_t *row_ptr, const int32_t *col, const float *eps, const float *T,
+                                 int64_t n, int32_t dim, float *E, hipStream_t s)
+{
+    int64_t blocks = (n + 255) / 256;
+    if (blocks > 65536) blocks = 65536;
+    if (blocks < 1) blocks = 1;
+    hipLaunchKernelGGL(k_init_transform, dim3((unsigned)blocks), dim3(256), 0, s, row_ptr, col, eps, T, n, dim, E);
+    return hipGetLastError();
+}
+
 // ---------------------------------------------------------------------------
 // One thread per vertex: the whole epoch for its row, term by term.
 // ---------------------------------------------------------------------------
@@ -71,19 +104,19 @@ __global__ __launch_bounds__(256) void k_epoch_rowwise(EpochArgs A, const int64_
             if (!edge_active(eps[e], A.epoch)) continue;
             ++cnt;
             float yj[DIM];
-            load_row<DIM>(A.E, (uint32_t)col[e], yj);
+            load_row<DIM>(A.T, (uint32_t)col[e], yj);
             long long fx[DIM];
-            attraction_fixed<DIM>(yi, yj, A.a, A.b, fx);
+            attraction_fixed<DIM>(yi, yj, A.a, A.b, A.attr_mult, fx);
 #pragma unroll
             for (int d = 0; d < DIM; ++d) acc[d] += fx[d];
             for (int32_t q = 0; 4 * q < A.neg_rate; ++q) {
                 Ctr w = negative_words(e, A.epoch, q, A.key_lo, A.key_hi);
                 for (int t = 0; t < 4 && 4 * q + t < A.neg_rate; ++t) {
                     const uint32_t k = word_to_vertex(t == 0 ? w.w[0] : t == 1 ? w.w[1] : t == 2 ? w.w[2] : w.w[3],
-                                                      A.n);
-                    if (k == i) continue;
+                                                      A.n_table);
+                    if (A.same_table && k == i) continue;
                     float yk[DIM];
-                    load_row<DIM>(A.E, k, yk);
+                    load_row<DIM>(A.T, k, yk);
                     repulsion_fixed<DIM>(yi, yk, A.a, A.b, fx);
 #pragma unroll
                     for (int d = 0; d < DIM; ++d) acc[d] += fx[d];
@@ -160,9 +193,11 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
     float *yrows = s_y[wv] + kHalo * DIM;   // row h of the wave at yrows[h * DIM], h in [-kHalo, nrows + kHalo)
     uint32_t *rec_n = s_rec[wv];
     const size_t g0 = (size_t)r0 * DIM;
-    // staged rows [lo, hi): the wave's own rows and up to kHalo on each side
-    const int64_t lo = r0 >= kHalo ? r0 - kHalo : 0;
-    const int64_t hi = r0 + nrows + kHalo <= (int64_t)A.n ? r0 + nrows + kHalo : (int64_t)A.n;
+    // staged rows [lo, hi): the wave's own rows and, when the tails index the
+    // same table, up to kHalo on each side
+    const int64_t halo = A.same_table ? kHalo : 0;
+    const int64_t lo = r0 >= halo ? r0 - halo : 0;
+    const int64_t hi = r0 + nrows + halo <= (int64_t)A.n ? r0 + nrows + halo : (int64_t)A.n;
     for (int t = lane; t < nrows * DIM; t += kWave) acc[t] = 0;
     for (int64_t t = (lo - r0) * DIM + lane; t < (hi - r0) * DIM; t += kWave) yrows[t] = A.E[(int64_t)g0 + t];
     if ((int)lane < kMaxPhases) rec_n[lane] = 0;
@@ -190,11 +225,11 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
     uint2 *q = s_q[wv];
     uint32_t qhead = 0, qtail = 0;
     auto file = [&](uint32_t u, uint32_t i, int h) {
-        const uint32_t k = word_to_vertex(u, A.n);
-        if (k == i) return;   // a draw equal to the source adds nothing
+        const uint32_t k = word_to_vertex(u, A.n_table);
+        if (A.same_table && k == i) return;   // a draw equal to the source adds nothing
         const uint32_t p = lg == 0 ? 0u : u >> (32 - lg);
         const uint32_t slot = atomicAdd(&rec_n[p], 1u);
-        if (slot < cap) rec_wave[(int64_t)p * cap + slot] = ((uint32_t)h << 24) | (k - range_base(p, lg, A.n));
+        if (slot < cap) rec_wave[(int64_t)p * cap + slot] = ((uint32_t)h << 24) | (k - range_base(p, lg, A.n_table));
         else atomicOr(G.overflow, 1u);
     };
     // attraction and negative draws of `count` queued sampled edges
@@ -208,14 +243,14 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
         float yi[DIM], yj[DIM];
 #pragma unroll
         for (int d = 0; d < DIM; ++d) yi[d] = yrows[h * DIM + d];
-        if ((int64_t)tail >= lo && (int64_t)tail < hi) {
+        if (A.same_table && (int64_t)tail >= lo && (int64_t)tail < hi) {
 #pragma unroll
             for (int d = 0; d < DIM; ++d) yj[d] = yrows[((int64_t)tail - r0) * DIM + d];
         } else {
-            load_row<DIM>(A.E, tail, yj);
+            load_row<DIM>(A.T, tail, yj);
         }
         long long fx[DIM];
-        attraction_fixed<DIM>(yi, yj, A.a, A.b, fx);
+        attraction_fixed<DIM>(yi, yj, A.a, A.b, A.attr_mult, fx);
         if (valid) {
 #pragma unroll
             for (int d = 0; d < DIM; ++d)
@@ -319,7 +354,7 @@ __global__ __launch_bounds__(256) void k_epoch_repulse(EpochArgs A, WaveGraph G,
     wave_sync();
 
     const uint32_t *recs = G.rec + roff + (int64_t)phase * cap;
-    const uint32_t base = range_base((uint32_t)phase, G.lg_phases, A.n);
+    const uint32_t base = range_base((uint32_t)phase, G.lg_phases, A.n_table);
     // kRepUnroll records per lane per step, all loads issued before use
     for (int64_t b = 0; b < nrec; b += kRepUnroll * kWave) {
         uint32_t r[kRepUnroll];
@@ -330,7 +365,7 @@ __global__ __launch_bounds__(256) void k_epoch_repulse(EpochArgs A, WaveGraph G,
         }
         float yi[kRepUnroll][DIM], yk[kRepUnroll][DIM];
 #pragma unroll
-        for (int u = 0; u < kRepUnroll; ++u) load_row<DIM>(A.E, base + (r[u] & 0xFFFFFFu), yk[u]);
+        for (int u = 0; u < kRepUnroll; ++u) load_row<DIM>(A.T, base + (r[u] & 0xFFFFFFu), yk[u]);
 #pragma unroll
         for (int u = 0; u < kRepUnroll; ++u) {
             const int h = (int)(r[u] >> 24);

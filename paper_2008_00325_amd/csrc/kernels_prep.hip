@@ -3,7 +3,8 @@
 //
 // Steps (all on the handle's stream, one host synchronisation at the end):
 //   1. check indices and values; w_max = largest weight of a candidate edge
-//      (val > 0, row != col)
+//      (val > 0, row != col; a bipartite graph -- new points to a frozen
+//      table -- keeps row == col, which are different vertices there)
 //   2. count kept edges per row (candidates with val >= w_max / n_epochs)
 //   3. exclusive scan of the counts -> row_ptr (int64), largest row
 //   4. scatter kept edges into their row's segment (order inside a row is
@@ -11,8 +12,8 @@
 //   5. sort each row by column with a rank sort (the rank of an entry is the
 //      number of smaller columns in its row; equal columns flag a duplicate),
 //      and compute eps = w_max / val
-//   6. symmetry: each kept (i, j, v) must find (j, i) with bit-equal v by
-//      binary search in row j
+//   6. symmetry (not for a bipartite graph): each kept (i, j, v) must find
+//      (j, i) with bit-equal v by binary search in row j
 //   7. wave partition for the epoch kernel
 #include "internal.hpp"
 
@@ -22,9 +23,16 @@ constexpr int kScanThreads = 256;
 constexpr int kScanItems = 8;
 constexpr int kScanTile = kScanThreads * kScanItems;
 
-__device__ __forceinline__ bool candidate(int32_t r, int32_t c, float v, uint32_t n)
+// rows in [0, n), columns in [0, n_cols); bipartite: row and column index
+// different vertex sets
+struct IngestShape {
+    uint32_t n, n_cols;
+    int32_t bipartite;
+};
+
+__device__ __forceinline__ bool candidate(int32_t r, int32_t c, float v, IngestShape sh)
 {
-    return (uint32_t)r < n && (uint32_t)c < n && r != c && v > 0.0f && isfinite(v);
+    return (uint32_t)r < sh.n && (uint32_t)c < sh.n_cols && (sh.bipartite || r != c) && v > 0.0f && isfinite(v);
 }
 
 __device__ __forceinline__ float keep_threshold(const PrepScalars *S, int32_t n_epochs)
@@ -47,7 +55,7 @@ __device__ __forceinline__ unsigned wave_max(unsigned v)
 }
 
 __global__ __launch_bounds__(256) void k_check_max(const int32_t *__restrict__ rows, const int32_t *__restrict__ cols,
-                                                   const float *__restrict__ vals, int64_t nnz, uint32_t n,
+                                                   const float *__restrict__ vals, int64_t nnz, IngestShape sh,
                                                    PrepScalars *S)
 {
     unsigned flags = 0, mx = 0;
@@ -55,9 +63,9 @@ __global__ __launch_bounds__(256) void k_check_max(const int32_t *__restrict__ r
     for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < nnz; t += stride) {
         int32_t r = rows[t], c = cols[t];
         float v = vals[t];
-        if ((uint32_t)r >= n || (uint32_t)c >= n) flags |= kBadIndex;
+        if ((uint32_t)r >= sh.n || (uint32_t)c >= sh.n_cols) flags |= kBadIndex;
         if (!isfinite(v)) flags |= kBadValue;
-        if (candidate(r, c, v, n)) mx = max(mx, __float_as_uint(v));  // positive floats order as integers
+        if (candidate(r, c, v, sh)) mx = max(mx, __float_as_uint(v));  // positive floats order as integers
     }
     flags = wave_or(flags);
     mx = wave_max(mx);
@@ -68,7 +76,7 @@ __global__ __launch_bounds__(256) void k_check_max(const int32_t *__restrict__ r
 }
 
 __global__ __launch_bounds__(256) void k_count(const int32_t *__restrict__ rows, const int32_t *__restrict__ cols,
-                                               const float *__restrict__ vals, int64_t nnz, uint32_t n,
+                                               const float *__restrict__ vals, int64_t nnz, IngestShape sh,
                                                int32_t n_epochs, const PrepScalars *S, int32_t *__restrict__ deg)
 {
     const float thresh = keep_threshold(S, n_epochs);
@@ -76,7 +84,7 @@ __global__ __launch_bounds__(256) void k_count(const int32_t *__restrict__ rows,
     for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < nnz; t += stride) {
         int32_t r = rows[t], c = cols[t];
         float v = vals[t];
-        if (candidate(r, c, v, n) && v >= thresh) atomicAdd(&deg[r], 1);
+        if (candidate(r, c, v, sh) && v >= thresh) atomicAdd(&deg[r], 1);
     }
 }
 
@@ -161,7 +169,7 @@ __global__ __launch_bounds__(kScanThreads) void k_scan_down(const int32_t *__res
 }
 
 __global__ __launch_bounds__(256) void k_scatter(const int32_t *__restrict__ rows, const int32_t *__restrict__ cols,
-                                                 const float *__restrict__ vals, int64_t nnz, uint32_t n,
+                                                 const float *__restrict__ vals, int64_t nnz, IngestShape sh,
                                                  int32_t n_epochs, const PrepScalars *S,
                                                  const int64_t *__restrict__ row_ptr, int32_t *__restrict__ cursor,
                                                  int32_t *__restrict__ trow, int32_t *__restrict__ tcol,
@@ -172,7 +180,7 @@ __global__ __launch_bounds__(256) void k_scatter(const int32_t *__restrict__ row
     for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < nnz; t += stride) {
         int32_t r = rows[t], c = cols[t];
         float v = vals[t];
-        if (candidate(r, c, v, n) && v >= thresh) {
+        if (candidate(r, c, v, sh) && v >= thresh) {
             int64_t p = row_ptr[r] + atomicAdd(&cursor[r], 1);
             trow[p] = r;
             tcol[p] = c;
@@ -250,21 +258,22 @@ int64_t scan_blocks(int64_t n) { return (n + kScanTile - 1) / kScanTile; }
 
 hipError_t launch_prep(const PrepBuffers &B, hipStream_t s)
 {
-    const uint32_t n = (uint32_t)B.n;
+    const IngestShape sh{(uint32_t)B.n, (uint32_t)B.n_cols, B.bipartite ? 1 : 0};
     const int64_t g = grid_for(B.nnz);
-    hipLaunchKernelGGL(k_check_max, dim3((unsigned)g), dim3(256), 0, s, B.rows, B.cols, B.vals, B.nnz, n, B.scalars);
-    hipLaunchKernelGGL(k_count, dim3((unsigned)g), dim3(256), 0, s, B.rows, B.cols, B.vals, B.nnz, n, B.n_epochs,
+    hipLaunchKernelGGL(k_check_max, dim3((unsigned)g), dim3(256), 0, s, B.rows, B.cols, B.vals, B.nnz, sh, B.scalars);
+    hipLaunchKernelGGL(k_count, dim3((unsigned)g), dim3(256), 0, s, B.rows, B.cols, B.vals, B.nnz, sh, B.n_epochs,
                        B.scalars, B.deg);
     const int64_t nb = B.nblocks_scan;
     hipLaunchKernelGGL(k_scan_reduce, dim3((unsigned)nb), dim3(kScanThreads), 0, s, B.deg, B.n, B.bsum, B.scalars);
     hipLaunchKernelGGL(k_scan_top, dim3(1), dim3(kScanThreads), 0, s, B.bsum, nb);
     hipLaunchKernelGGL(k_scan_down, dim3((unsigned)nb), dim3(kScanThreads), 0, s, B.deg, B.n, B.bsum, B.row_ptr, nb);
-    hipLaunchKernelGGL(k_scatter, dim3((unsigned)g), dim3(256), 0, s, B.rows, B.cols, B.vals, B.nnz, n, B.n_epochs,
+    hipLaunchKernelGGL(k_scatter, dim3((unsigned)g), dim3(256), 0, s, B.rows, B.cols, B.vals, B.nnz, sh, B.n_epochs,
                        B.scalars, B.row_ptr, B.cursor, B.trow, B.tcol, B.tval);
     hipLaunchKernelGGL(k_row_sort, dim3((unsigned)g), dim3(256), 0, s, B.trow, B.tcol, B.tval, B.row_ptr, B.n,
                        B.scalars, B.col, B.sval, B.eps);
-    hipLaunchKernelGGL(k_symmetry, dim3((unsigned)g), dim3(256), 0, s, B.trow, B.col, B.sval, B.row_ptr, B.n,
-                       B.scalars);
+    if (!B.bipartite)
+        hipLaunchKernelGGL(k_symmetry, dim3((unsigned)g), dim3(256), 0, s, B.trow, B.col, B.sval, B.row_ptr, B.n,
+                           B.scalars);
     return hipGetLastError();
 }
 

@@ -101,9 +101,13 @@ __device__ __forceinline__ float repulsion_coef(float d2, float a, float b)
 }
 
 struct EpochArgs {
-    const float *E;      // snapshot E_n, n x DIM
+    const float *E;      // snapshot E_n of the moving vertices, n x DIM
     float *E_next;       // E_{n+1}
+    const float *T;      // table of tails and negative samples: E itself, or a frozen layout (transform)
     uint32_t n;
+    uint32_t n_table;    // rows of T; negative samples are drawn from [0, n_table)
+    int32_t same_table;  // T is E: a draw equal to the source is skipped, near tails may come from LDS
+    float attr_mult;     // 2 when the reverse edge's equal share lands on the row too (symmetric B), else 1
     int32_t epoch;
     int32_t neg_rate;
     float a, b;
@@ -143,19 +147,20 @@ __device__ __forceinline__ long long to_fixed(float t)
     return (long long)(__double_as_longlong(y) - __double_as_longlong(shifter));
 }
 
-// Attraction share of vertex i for a sampled edge (i -> j): twice the clipped
-// gradient of log Phi -- its own "move the source" share plus the equal share
-// of the reverse edge (j -> i), which is sampled in the same epochs because B
-// is symmetric with bit-equal weights.
+// Attraction share of vertex i for a sampled edge (i -> j): `mult` times the
+// clipped gradient of log Phi.  In a fit mult = 2: the row's own "move the
+// source" share plus the equal share of the reverse edge (j -> i), which is
+// sampled in the same epochs because B is symmetric with bit-equal weights.
+// In a transform (j frozen, no reverse edge) mult = 1.
 template <int DIM>
 __device__ __forceinline__ void attraction_fixed(const float (&yi)[DIM], const float (&yj)[DIM], float a, float b,
-                                                 long long (&fx)[DIM])
+                                                 float mult, long long (&fx)[DIM])
 {
     float diff[DIM];
     const float d2 = sq_dist<DIM>(yi, yj, diff);
     const float c = attraction_coef(d2, a, b);
 #pragma unroll
-    for (int d = 0; d < DIM; ++d) fx[d] = to_fixed(2.0f * clip4(c * diff[d]));
+    for (int d = 0; d < DIM; ++d) fx[d] = to_fixed(mult * clip4(c * diff[d]));
 }
 
 // Repulsion of vertex i from a negative sample k (callers skip k == i).

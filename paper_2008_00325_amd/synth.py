@@ -177,3 +177,14 @@ def random_symmetric_coo(n: int, avg_deg: int, seed: int, shuffle: bool = True):
         p = rng.permutation(rows.size)
         rows, cols, vals = rows[p], cols[p], vals[p]
     return rows, cols, vals
+
+
+def quality_sample(n: int, rows: int = 10_000, negatives: int = 64, seed: int = 12345):
+    """Seeded vertex sample for the quality measures of graph-only workloads:
+    `rows` distinct vertices (sorted) and, for each, `negatives` vertices drawn
+    uniformly from [0, n) (the fixed stand-ins of the objective's random
+    negative samples)."""
+    rng = np.random.default_rng(seed)
+    r = np.sort(rng.choice(n, size=min(rows, n), replace=False)).astype(np.int64)
+    neg = rng.integers(0, n, size=(r.size, negatives), dtype=np.int64)
+    return r, neg

@@ -28,7 +28,8 @@ UMAP_MODE_SYNC = 0
 UMAP_MODE_ASYNC = 1
 
 EXPORTS = (
-    "umap_layout_create", "umap_layout_create_device", "umap_layout_run", "umap_layout_run_epochs",
+    "umap_layout_create", "umap_layout_create_device", "umap_transform_create", "umap_layout_run",
+    "umap_layout_init", "umap_layout_run_epochs",
     "umap_layout_get", "umap_layout_get_device", "umap_layout_set_embedding", "umap_layout_get_graph",
     "umap_layout_stats", "umap_layout_set_stream", "umap_layout_destroy", "umap_layout_last_error",
     "umap_layout_debug_active", "umap_layout_debug_negatives", "umap_layout_set_kernel", "umap_layout_set_mode",
@@ -84,7 +85,9 @@ def lib() -> ctypes.CDLL:
         sig = {
             "umap_layout_create": [PP, i64, i32, P, P, P, i64, f32, f32, i32, i32],
             "umap_layout_create_device": [PP, i64, i32, P, P, P, i64, f32, f32, i32, i32, P],
+            "umap_transform_create": [PP, i64, i32, P, i64, P, P, P, i64, f32, f32, i32, i32],
             "umap_layout_run": [P, u64],
+            "umap_layout_init": [P, u64],
             "umap_layout_run_epochs": [P, u64, i32, i32],
             "umap_layout_get": [P, P],
             "umap_layout_get_device": [P, P],
@@ -188,6 +191,22 @@ def umap_layout_create(n: int, n_components: int, rows, cols, vals, a: float, b:
     return Handle(out, n, n_components)
 
 
+def umap_transform_create(n_new: int, table, rows, cols, vals, a: float, b: float, n_epochs: int,
+                          neg_rate: int) -> Handle:
+    t = _host(table, np.float32)
+    if t.ndim != 2:
+        raise ValueError("table must be an n_table x n_components array")
+    r = _host(rows, np.int32)
+    c = _host(cols, np.int32)
+    v = _host(vals, np.float32)
+    if not (r.size == c.size == v.size):
+        raise ValueError("rows, cols and vals must have the same length")
+    out = ctypes.c_void_p()
+    _check(lib().umap_transform_create(ctypes.byref(out), n_new, t.shape[1], _hp(t), t.shape[0], _hp(r), _hp(c),
+                                       _hp(v), r.size, a, b, n_epochs, neg_rate))
+    return Handle(out, n_new, t.shape[1])
+
+
 def umap_layout_create_device(n: int, n_components: int, rows, cols, vals, nnz: int, a: float, b: float,
                               n_epochs: int, neg_rate: int, stream=None) -> Handle:
     out = ctypes.c_void_p()
@@ -198,6 +217,10 @@ def umap_layout_create_device(n: int, n_components: int, rows, cols, vals, nnz: 
 
 def umap_layout_run(h: Handle, seed: int) -> None:
     _check(lib().umap_layout_run(h.ptr, seed))
+
+
+def umap_layout_init(h: Handle, seed: int) -> None:
+    _check(lib().umap_layout_init(h.ptr, seed))
 
 
 def umap_layout_run_epochs(h: Handle, seed: int, first: int, last: int) -> None:

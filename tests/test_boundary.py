@@ -28,7 +28,7 @@ def _declared():
 
 def test_every_declared_function_is_exported(L):
     names = _declared()
-    assert len(names) == 21
+    assert len(names) == 23
     for name in names:
         assert hasattr(L, name), name
         assert name in U.EXPORTS
@@ -82,6 +82,7 @@ def test_create_device_rejects_scalars_without_touching_the_gpu(L):
 
 def test_null_handles_are_rejected(L):
     assert L.umap_layout_run(None, 1) == U.UMAP_E_INVAL
+    assert L.umap_layout_init(None, 1) == U.UMAP_E_INVAL
     assert L.umap_layout_run_epochs(None, 1, 0, 1) == U.UMAP_E_INVAL
     assert L.umap_layout_get(None, None) == U.UMAP_E_INVAL
     assert L.umap_layout_get_device(None, None) == U.UMAP_E_INVAL
@@ -116,6 +117,34 @@ def test_fuzzy_graph_and_probe_argument_checks(L):
     assert L.umap_trustworthiness(None, 100, 4, p, 2, 15, ctypes.byref(out), None) == U.UMAP_E_INVAL
     assert L.umap_trustworthiness(p, 100, 4, p, 2, 15, None, None) == U.UMAP_E_INVAL
     assert out.value == 7.0
+
+
+def test_transform_create_argument_checks(L):
+    """Every check of umap_transform_create runs before a HIP call."""
+    T = np.zeros((5, 2), np.float32)
+    r = np.array([0, 1], np.int32)
+    c = np.array([4, 4], np.int32)
+    v = np.ones(2, np.float32)
+    P = ctypes.c_void_p
+    out = P()
+
+    def call(n_new=3, table=T, n_table=5, rows=r, cols=c, vals=v, dim=2, nnz=2, a=1.0, b=1.0, N=10, R=5,
+             outp=ctypes.byref(out)):
+        tp = None if table is None else table.ctypes.data_as(P)
+        return L.umap_transform_create(outp, n_new, dim, tp, n_table, rows.ctypes.data_as(P),
+                                       cols.ctypes.data_as(P), vals.ctypes.data_as(P), nnz, a, b, N, R)
+
+    assert call(outp=None) == U.UMAP_E_INVAL
+    assert call(n_new=0) == U.UMAP_E_INVAL
+    assert call(n_table=0) == U.UMAP_E_INVAL
+    assert call(table=None) == U.UMAP_E_INVAL
+    assert call(dim=17) == U.UMAP_E_INVAL
+    assert call(table=np.array([[0, 0], [0, np.inf], [0, 0], [0, 0], [0, 0]], np.float32)) == U.UMAP_E_INVAL
+    assert call(cols=np.array([4, 5], np.int32)) == U.UMAP_E_INVAL     # column beyond the table
+    assert call(rows=np.array([0, 3], np.int32)) == U.UMAP_E_INVAL     # row beyond the new points
+    assert call(vals=np.array([1, np.nan], np.float32)) == U.UMAP_E_INVAL
+    assert call(N=0) == U.UMAP_E_INVAL
+    assert not out.value
 
 
 def test_fit_ab_matches_oracle(orc):

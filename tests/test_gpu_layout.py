@@ -272,6 +272,54 @@ def test_single_epoch_other_full_sizes(name):
                       f"{name} scale 10")
 
 
+def _window_quality_golden():
+    import json
+    import os
+
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "window_quality.json")
+    with open(path) as f:
+        return json.load(f)
+
+
+@pytest.mark.parametrize("name,mode", [("window1m", 0), ("window1m", 1), ("window1m_k30", 0), ("window5m", 0)])
+def test_full_run_quality_window(name, mode):
+    """Full 200-epoch runs of the graph-only workloads, scored like the oracle's
+    stored runs (same seed, same sample): recall@15 within 0.01 and the
+    objective within 1 % of the oracle's.  The asynchronous mode is held to the
+    same bounds."""
+    import torch
+
+    gold = _window_quality_golden()
+    ref = gold[name]
+    seed = gold["seed"]
+    w = synth.WORKLOADS[name]
+    case(f"{name} mode {mode}: building the graph on the host")
+    ids, dist = synth.workload_knn(w)
+    r, c, v = O.fuzzy_graph(ids, dist)
+    del dist
+    g = O.prep(w.n, r, c, v, w.n_epochs)
+    a, b = O.fit_ab(w.spread, w.min_dist)
+    dr, dc, dv = (torch.from_numpy(x).cuda() for x in (r, c, v))
+    nnz = r.size
+    del r, c, v
+    case(f"{name} mode {mode}: GPU run")
+    with U.umap_layout_create_device(w.n, w.dim, dr, dc, dv, nnz, a, b, w.n_epochs, w.neg_rate) as h:
+        del dr, dc, dv
+        U.umap_layout_set_mode(h, mode)
+        U.umap_layout_run(h, seed)
+        E = U.umap_layout_get(h)
+        st = U.umap_layout_stats(h)
+    assert st["active_edges"] == ref["active_edges"]
+    assert np.all(np.isfinite(E))
+    rows, neg = synth.quality_sample(w.n)
+    rec = O.recall_at_k(ids, E, rows, 15)
+    obj = O.objective(g, E, a, b, w.neg_rate, rows, neg)
+    print(f"  recall@15 {rec:.4f} (oracle {ref['recall15']:.4f}, init {ref['recall15_init']:.4f}); "
+          f"objective {obj:.6g} (oracle {ref['objective']:.6g}, init {ref['objective_init']:.6g})", flush=True)
+    assert abs(rec - ref["recall15"]) <= 0.01
+    assert abs(obj - ref["objective"]) <= 0.01 * ref["objective"]
+
+
 @pytest.mark.parametrize("dim,R,N", [(1, 5, 20), (3, 5, 200), (4, 0, 50), (16, 7, 30)])
 def test_single_epoch_dims_and_rates(dim, R, N):
     n = 5003
