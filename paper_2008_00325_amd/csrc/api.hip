@@ -355,7 +355,10 @@ int run_epochs_impl(umap_layout *h, uint64_t seed, int32_t first, int32_t last, 
     if (async && (int64_t)h->max_degree + ul::kWaveCost >= ((int64_t)1 << 24))
         return fail(UMAP_E_INVAL, "the asynchronous mode needs rows of fewer than %d edges",
                     (1 << 24) - ul::kWaveCost);
-    const int kernel = async ? 2 : fits ? h->kernel : 1;
+    // epoch kernel: 0 edge-parallel, 1 one thread per vertex, kAsyncKernel the
+    // asynchronous mode
+    constexpr int kAsyncKernel = -1;
+    const int kernel = async ? kAsyncKernel : fits ? h->kernel : 1;
     const bool records = kernel == 0;
     const int cur0 = h->cur;
     const size_t nd_bytes = sizeof(float) * (size_t)h->n * (size_t)h->dim;
@@ -380,7 +383,7 @@ int run_epochs_impl(umap_layout *h, uint64_t seed, int32_t first, int32_t last, 
             A.epoch = ep;
             A.alpha = 1.0 - (double)ep / (double)h->n_epochs;
             A.counts = h->counts + (int64_t)((ep - pending_from) % ring) * h->count_stride;
-            if (which == 2) {
+            if (which == kAsyncKernel) {
                 A.E = A.E_next = h->E[h->cur];   // in place
                 A.T = A.E;
                 UL_HIP(ul::launch_epoch_hogwild(h->dim, A, G, h->stream));

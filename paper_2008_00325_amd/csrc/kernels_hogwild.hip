@@ -70,7 +70,7 @@ __global__ __launch_bounds__(256) void k_epoch_hogwild(EpochArgs A, WaveGraph G)
     uint32_t qhead = 0, qtail = 0;
     int64_t qn = 0;
 
-    auto process = [&](int count) {
+    auto process = [&](int count) __attribute__((always_inline)) {
         const bool valid = (int)lane < count;
         const uint2 ent = q[(qhead + lane) & (kHwQueue - 1)];
         const int h = valid ? (int)(ent.y >> 24) : 0;
@@ -83,12 +83,15 @@ __global__ __launch_bounds__(256) void k_epoch_hogwild(EpochArgs A, WaveGraph G)
         float yi[DIM], yj[DIM];
 #pragma unroll
         for (int d = 0; d < DIM; ++d) yi[d] = yrows[h * DIM + d] + acc[h * DIM + d];
-        if ((int64_t)tail >= lo && (int64_t)tail < hi) {
+        // staged copy (plus pending changes for the wave's own rows) when j is
+        // staged, else the table; the LDS reads are unconditional (a valid row
+        // otherwise) so that they never merge with the global read
+        const bool near = (int64_t)tail >= lo && (int64_t)tail < hi;
+        const int64_t jn = near ? jt : 0;
+        const int64_t ja = j_own ? jt : 0;
 #pragma unroll
-            for (int d = 0; d < DIM; ++d) yj[d] = yrows[jt * DIM + d] + (j_own ? acc[jt * DIM + d] : 0.0f);
-        } else {
-            load_row<DIM>(E, tail, yj);
-        }
+        for (int d = 0; d < DIM; ++d) yj[d] = yrows[jn * DIM + d] + (j_own ? acc[ja * DIM + d] : 0.0f);
+        if (!near) load_row<DIM>(E, tail, yj);
 
         // negative samples: every y_k is loaded before the sequential updates
         constexpr int kNeg = NQ > 0 ? 4 * NQ : 1;
@@ -112,7 +115,7 @@ __global__ __launch_bounds__(256) void k_epoch_hogwild(EpochArgs A, WaveGraph G)
             g[d] = clip4(ca * diff[d]);
             cur[d] = fmaf(alpha, g[d], yi[d]);
         }
-        auto repel = [&](const float (&y)[DIM]) {
+        auto repel = [&](const float (&y)[DIM]) __attribute__((always_inline)) {
             float df[DIM];
             const float dd = sq_dist<DIM>(cur, y, df);
             const float cr = repulsion_coef(dd, A.a, A.b);
@@ -158,7 +161,7 @@ __global__ __launch_bounds__(256) void k_epoch_hogwild(EpochArgs A, WaveGraph G)
 
     if (e1 > e0) {
         // one chunk of 64 edges in flight while the previous one is classified
-        auto load = [&](int64_t base, float &ev, int32_t &cv, uint8_t &hv) {
+        auto load = [&](int64_t base, float &ev, int32_t &cv, uint8_t &hv) __attribute__((always_inline)) {
             int64_t e = base + lane;
             e = e < e1 ? e : e1 - 1;
             ev = G.eps[e];

@@ -138,11 +138,12 @@ __global__ __launch_bounds__(256) void k_epoch_rowwise(EpochArgs A, const int64_
 // k_epoch_draw launch followed by P k_epoch_repulse launches:
 //  * k_epoch_draw streams eps (and col, and each edge's row inside the wave)
 //    over the wave's edges, classifies every edge for this epoch and appends
-//    the sampled ones -- compacted with a ballot -- to the wave's slice of a
-//    scratch list.  It then takes the list 64 edges at a time: each lane adds
-//    its edge's attraction to the wave's LDS accumulator, draws the edge's
-//    negative samples and files each one as a 4-byte record under the range
-//    of the vertex table it falls in.  The accumulator goes to delta.
+//    the sampled ones -- compacted with a ballot -- to an LDS ring.  It takes
+//    the ring 64 edges at a time: each lane adds its edge's attraction to the
+//    wave's LDS accumulator (y_j from the staged halo rows when j is near),
+//    draws the edge's negative samples and files each one as a 4-byte record
+//    under the range of the vertex table it falls in.  The accumulator goes
+//    to delta.
 //  * k_epoch_repulse (range p) reads the wave's records of range p and adds
 //    their repulsions.  All gathers of one launch hit one 1/P slice of the
 //    vertex table, which is sized to stay resident in an XCD's L2.  The last
@@ -206,7 +207,8 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
     int64_t qn = 0;
     // loads are unconditional (the index is clamped into the wave's range and
     // the value masked) so that the next super-chunk stays in flight
-    auto load_super = [&](int64_t sbase, float (&ev)[kSuper], int32_t (&cv)[kSuper], uint8_t (&hv)[kSuper]) {
+    auto load_super = [&](int64_t sbase, float (&ev)[kSuper], int32_t (&cv)[kSuper],
+                          uint8_t (&hv)[kSuper]) __attribute__((always_inline)) {
 #pragma unroll
         for (int j = 0; j < kSuper; ++j) {
             int64_t e = sbase + j * kWave + lane;
@@ -224,7 +226,7 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
     uint32_t *const rec_wave = G.rec + roff;   // this wave's slots, range p from p * cap
     uint2 *q = s_q[wv];
     uint32_t qhead = 0, qtail = 0;
-    auto file = [&](uint32_t u, uint32_t i, int h) {
+    auto file = [&](uint32_t u, uint32_t i, int h) __attribute__((always_inline)) {
         const uint32_t k = word_to_vertex(u, A.n_table);
         if (A.same_table && k == i) return;   // a draw equal to the source adds nothing
         const uint32_t p = lg == 0 ? 0u : u >> (32 - lg);
@@ -233,7 +235,7 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
         else atomicOr(G.overflow, 1u);
     };
     // attraction and negative draws of `count` queued sampled edges
-    auto process = [&](int count) {
+    auto process = [&](int count) __attribute__((always_inline)) {
         const bool valid = (int)lane < count;
         const uint2 ent = q[(qhead + lane) & (kQueue - 1)];
         const int h = valid ? (int)(ent.y >> 24) : 0;
@@ -243,18 +245,22 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
         float yi[DIM], yj[DIM];
 #pragma unroll
         for (int d = 0; d < DIM; ++d) yi[d] = yrows[h * DIM + d];
-        if (A.same_table && (int64_t)tail >= lo && (int64_t)tail < hi) {
+        // y_j from the staged rows when j is one of them, else from the table;
+        // the LDS read is unconditional (a valid row otherwise) so that the
+        // two reads never merge into one generic-address load
+        const bool near = A.same_table && (int64_t)tail >= lo && (int64_t)tail < hi;
+        const int64_t jt = near ? (int64_t)tail - r0 : 0;
 #pragma unroll
-            for (int d = 0; d < DIM; ++d) yj[d] = yrows[((int64_t)tail - r0) * DIM + d];
-        } else {
-            load_row<DIM>(A.T, tail, yj);
-        }
+        for (int d = 0; d < DIM; ++d) yj[d] = yrows[jt * DIM + d];
+        if (!near) load_row<DIM>(A.T, tail, yj);
         long long fx[DIM];
         attraction_fixed<DIM>(yi, yj, A.a, A.b, A.attr_mult, fx);
         if (valid) {
 #pragma unroll
             for (int d = 0; d < DIM; ++d)
                 atomicAdd(reinterpret_cast<unsigned long long *>(&acc[h * DIM + d]), (unsigned long long)fx[d]);
+        }
+        if (valid) {
             if constexpr (NQ >= 0) {
                 uint32_t u[4 * NQ > 0 ? 4 * NQ : 1];
                 if constexpr (NQ > 0) negative_words_all<NQ>(e, A.epoch, A.key_lo, A.key_hi, u);
@@ -273,7 +279,7 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
         qhead += (uint32_t)count;
     };
     auto scan_super = [&](int64_t sbase, const float (&ev)[kSuper], const int32_t (&cv)[kSuper],
-                          const uint8_t (&hv)[kSuper]) {
+                          const uint8_t (&hv)[kSuper]) __attribute__((always_inline)) {
 #pragma unroll
         for (int j = 0; j < kSuper; ++j) {
             const int64_t e = sbase + j * kWave + lane;

@@ -238,10 +238,12 @@ def test_single_epoch_window1m_full_size(window1m_graph):
     dr, dc, dv = (torch.from_numpy(x).cuda() for x in (r, c, v))
     with U.umap_layout_create_device(w.n, w.dim, dr, dc, dv, r.size, a, b, w.n_epochs, w.neg_rate) as h:
         _check_graph(h, g)
-        for scale, seed in ((10.0, 3), (0.5, 4)):
-            E = synth.embedding_state(w.n, w.dim, seed, scale)
-            _epoch_parity(h, g, E, (0, 1, w.n_epochs // 2, w.n_epochs - 1), a, b, w.n_epochs, w.neg_rate, 11,
-                          f"window1m scale {scale}")
+        for kernel in (0, 1):
+            U.umap_layout_set_kernel(h, kernel)
+            for scale, seed in ((10.0, 3), (0.5, 4)):
+                E = synth.embedding_state(w.n, w.dim, seed, scale)
+                _epoch_parity(h, g, E, (0, 1, w.n_epochs // 2, w.n_epochs - 1), a, b, w.n_epochs, w.neg_rate, 11,
+                              f"window1m kernel {kernel} scale {scale}")
 
 
 @pytest.mark.parametrize("name", ["window1m_k30", "window5m"])
@@ -268,8 +270,10 @@ def test_single_epoch_other_full_sizes(name):
         case(f"{name}: {st['table_ranges']} table ranges, {st['nnz_kept']} edges")
         assert st["table_ranges"] == (8 if w.dim == 3 else 16)
         E = synth.embedding_state(w.n, w.dim, 6, 10.0)
-        _epoch_parity(h, g, E, (0, 1, w.n_epochs // 2, w.n_epochs - 1), a, b, w.n_epochs, w.neg_rate, 13,
-                      f"{name} scale 10")
+        for kernel in (0, 1):
+            U.umap_layout_set_kernel(h, kernel)
+            _epoch_parity(h, g, E, (0, 1, w.n_epochs // 2, w.n_epochs - 1), a, b, w.n_epochs, w.neg_rate, 13,
+                          f"{name} kernel {kernel} scale 10")
 
 
 def _window_quality_golden():
