@@ -167,7 +167,10 @@ __device__ __forceinline__ uint32_t range_base(uint32_t p, int32_t lg, uint32_t 
     return lg == 0 ? 0u : __umulhi(p << (32 - lg), n);
 }
 
-template <int DIM, int NQ>
+// FIT: the tails and negatives index the moving layout itself (a fit: halo
+// rows in LDS, self draws skipped, both shares of the attraction); else they
+// index a frozen table (a transform).
+template <int DIM, int NQ, bool FIT>
 __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
 {
     constexpr int CAP = rows_cap(DIM);
@@ -196,7 +199,7 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
     const size_t g0 = (size_t)r0 * DIM;
     // staged rows [lo, hi): the wave's own rows and, when the tails index the
     // same table, up to kHalo on each side
-    const int64_t halo = A.same_table ? kHalo : 0;
+    constexpr int64_t halo = FIT ? kHalo : 0;
     const int64_t lo = r0 >= halo ? r0 - halo : 0;
     const int64_t hi = r0 + nrows + halo <= (int64_t)A.n ? r0 + nrows + halo : (int64_t)A.n;
     for (int t = lane; t < nrows * DIM; t += kWave) acc[t] = 0;
@@ -228,7 +231,7 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
     uint32_t qhead = 0, qtail = 0;
     auto file = [&](uint32_t u, uint32_t i, int h) __attribute__((always_inline)) {
         const uint32_t k = word_to_vertex(u, A.n_table);
-        if (A.same_table && k == i) return;   // a draw equal to the source adds nothing
+        if (FIT && k == i) return;   // a draw equal to the source adds nothing
         const uint32_t p = lg == 0 ? 0u : u >> (32 - lg);
         const uint32_t slot = atomicAdd(&rec_n[p], 1u);
         if (slot < cap) rec_wave[(int64_t)p * cap + slot] = ((uint32_t)h << 24) | (k - range_base(p, lg, A.n_table));
@@ -248,13 +251,13 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
         // y_j from the staged rows when j is one of them, else from the table;
         // the LDS read is unconditional (a valid row otherwise) so that the
         // two reads never merge into one generic-address load
-        const bool near = A.same_table && (int64_t)tail >= lo && (int64_t)tail < hi;
+        const bool near = FIT && (int64_t)tail >= lo && (int64_t)tail < hi;
         const int64_t jt = near ? (int64_t)tail - r0 : 0;
 #pragma unroll
         for (int d = 0; d < DIM; ++d) yj[d] = yrows[jt * DIM + d];
         if (!near) load_row<DIM>(A.T, tail, yj);
         long long fx[DIM];
-        attraction_fixed<DIM>(yi, yj, A.a, A.b, A.attr_mult, fx);
+        attraction_fixed<DIM>(yi, yj, A.a, A.b, FIT ? 2.0f : 1.0f, fx);
         if (valid) {
 #pragma unroll
             for (int d = 0; d < DIM; ++d)
@@ -418,7 +421,10 @@ static hipError_t launch_epoch_dq(int kernel, const EpochArgs &A, const WaveGrap
     }
     const int64_t blocks = (G.n_waves + kWavesPerBlock - 1) / kWavesPerBlock;
     const int64_t grid = ((blocks + 7) / 8) * 8;
-    hipLaunchKernelGGL((k_epoch_draw<DIM, NQ>), dim3((unsigned)grid), dim3(256), 0, s, A, G);
+    if (A.same_table)
+        hipLaunchKernelGGL((k_epoch_draw<DIM, NQ, true>), dim3((unsigned)grid), dim3(256), 0, s, A, G);
+    else
+        hipLaunchKernelGGL((k_epoch_draw<DIM, NQ, false>), dim3((unsigned)grid), dim3(256), 0, s, A, G);
     for (int32_t p = 0; p < G.n_phases; ++p)
         hipLaunchKernelGGL((k_epoch_repulse<DIM>), dim3((unsigned)grid), dim3(256), 0, s, A, G, p);
     return hipGetLastError();

@@ -289,8 +289,8 @@ def _window_quality_golden():
 def test_full_run_quality_window(name, mode):
     """Full 200-epoch runs of the graph-only workloads, scored like the oracle's
     stored runs (same seed, same sample): recall@15 within 0.01 and the
-    objective within 1 % of the oracle's.  The asynchronous mode is held to the
-    same bounds."""
+    objective within 1 % of the oracle's.  The asynchronous mode (a different
+    trajectory, not the oracle's) must be no worse by the same margins."""
     import torch
 
     gold = _window_quality_golden()
@@ -322,8 +322,15 @@ def test_full_run_quality_window(name, mode):
     obj = O.objective(g, E, a, b, w.neg_rate, rows, neg)
     print(f"  recall@15 {rec:.4f} (oracle {ref['recall15']:.4f}, init {ref['recall15_init']:.4f}); "
           f"objective {obj:.6g} (oracle {ref['objective']:.6g}, init {ref['objective_init']:.6g})", flush=True)
-    assert abs(rec - ref["recall15"]) <= 0.01
-    assert abs(obj - ref["objective"]) <= 0.01 * ref["objective"]
+    if mode == U.UMAP_MODE_SYNC:
+        assert abs(rec - ref["recall15"]) <= 0.01
+        assert abs(obj - ref["objective"]) <= 0.01 * ref["objective"]
+    else:
+        # in-place updates let later edges of an epoch see earlier moves: the
+        # asynchronous run may converge further than the oracle's synchronous
+        # one, so its bound is one-sided (no worse than the oracle's)
+        assert rec >= ref["recall15"] - 0.01
+        assert obj <= 1.01 * ref["objective"]
 
 
 @pytest.mark.parametrize("dim,R,N", [(1, 5, 20), (3, 5, 200), (4, 0, 50), (16, 7, 30)])
