@@ -218,14 +218,27 @@ def cpu_baseline(w, ids, dist, budget_s: float = 12.0):
         done.append(ep)
         if spent > budget_s:
             break
+    cores = O.num_threads()
+    # one thread on the middle epoch of the run
+    mid = w.n_epochs // 2
+    O.set_num_threads(1)
+    try:
+        t1 = time.perf_counter()
+        _, act1 = O.epoch(g, E, mid, a, b, w.n_epochs, w.neg_rate, 0)
+        one = act1 * (1 + w.neg_rate) / (time.perf_counter() - t1)
+    finally:
+        O.set_num_threads(cores)
+    log(f"oracle: {updates / spent:.3g} edge-updates/s on {cores} threads, {one:.3g} on one")
     return {
         "value": updates / spent,
         "unit": "edge-updates/s",
-        "cores": O.num_threads(),
+        "cores": cores,
         "kind": "oracle",
         "sample": f"{len(done)} of the {w.n_epochs} epochs of the {w.name} layout (spread over the run: "
                   f"{done[:6]}...), each from the random initial layout; fp64 push form, "
                   f"{updates} edge updates in {spent:.2f} s",
+        "single_thread_value": one,
+        "single_thread_sample": f"epoch {mid} from the random initial layout on one thread",
     }
 
 

@@ -228,8 +228,8 @@ int umap_layout_debug_active(const umap_layout *h, int32_t epoch, uint8_t *out);
 
 /* umap_layout_debug_negatives -- host array of count x neg_rate uint32: the
  * negative-sample vertices the epoch kernel draws for edges
- * e_first .. e_first + count - 1 in `epoch` with `seed`, computed on the device
- * by the same routine.  0 <= e_first, e_first + count <= nnz_kept.  Blocking. */
+ * e_first .. e_first + count - 1 in `epoch` with `seed` (vertices of the
+ * table for a transform handle), computed on the device by the same routine.  0 <= e_first, e_first + count <= nnz_kept.  Blocking. */
 int umap_layout_debug_negatives(const umap_layout *h, uint64_t seed, int32_t epoch, int64_t e_first,
                                 int64_t count, uint32_t *out);
 

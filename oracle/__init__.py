@@ -71,6 +71,7 @@ def lib() -> ctypes.CDLL:
         L.orc_epoch_rows.argtypes = [i64, i32, P, P, P, f64, f64, i32, i32, u64, i32, P, i64, P, P]
         L.orc_run.argtypes = [i64, i32, P, P, P, f64, f64, i32, i32, u64, P, P]
         L.orc_num_threads.restype = ctypes.c_int
+        L.orc_set_num_threads.argtypes = [i32]
         _lib = L
     return _lib
 
@@ -85,6 +86,11 @@ def _c(a, dtype):
 
 def num_threads() -> int:
     return int(lib().orc_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """Threads of the oracle's later parallel regions (results do not depend on it)."""
+    lib().orc_set_num_threads(n)
 
 
 # --------------------------------------------------------------------------

@@ -551,3 +551,14 @@ int orc_num_threads(void)
     return 1;
 #endif
 }
+
+/* Threads of later parallel regions (the sums are reduced in a fixed chunk
+ * order, so the results do not depend on it). */
+void orc_set_num_threads(int n)
+{
+#ifdef _OPENMP
+    if (n > 0) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}

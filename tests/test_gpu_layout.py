@@ -387,6 +387,12 @@ def test_resume_equals_uninterrupted(blobs_graph):
         U.umap_layout_set_embedding(h2, mid)
         U.umap_layout_run_epochs(h2, 5, 23, N)
         assert np.array_equal(U.umap_layout_get(h2).view(np.uint32), full.view(np.uint32))
+        # init, then the epochs in two pieces, equals one run
+        U.umap_layout_init(h2, 5)
+        assert np.array_equal(U.umap_layout_get(h2), O.init_layout(w.n, 2, 5))
+        U.umap_layout_run_epochs(h2, 5, 0, 40)
+        U.umap_layout_run_epochs(h2, 5, 40, N)
+        assert np.array_equal(U.umap_layout_get(h2).view(np.uint32), full.view(np.uint32))
 
 
 def test_full_run_trustworthiness(blobs_graph):

@@ -116,6 +116,9 @@ def test_transform_epoch_parity_large_table(n_table, dim):
     with U.umap_transform_create(n_new, T, rows, cols, vals, a, b, N, R) as h:
         _check_graph(h, g)
         assert U.umap_layout_stats(h)["table_ranges"] == 4
+        # negatives are drawn from the table's rows
+        got = U.umap_layout_debug_negatives(h, 9, 7, 1000, 5000)
+        assert np.array_equal(got, O.negative_vertices(9, 7, 1000, 5000, R, n_table))
         states = [synth.embedding_state(n_new, dim, 13, 10.0)]
         _epoch_parity(h, g, T, states, (0, N // 2, N - 1), a, b, N, R, 9, f"table {n_table} x {dim}")
 
