@@ -34,6 +34,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
+FP32_MFMA_PEAK_TFLOPS = 157.3   # MI355X dense fp32 matrix peak
 # HBM traffic of one epoch from rocprofv3 FETCH_SIZE / WRITE_SIZE passes (scaled by the
 # same counters on the library's copy probe); valid while the kernel sources hash the same
 PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "epoch_window1m.md")
@@ -94,7 +95,13 @@ def build_input(w, torch, U):
     cols = torch.empty_like(rows)
     vals = torch.empty(2 * n * k, dtype=torch.float32, device="cuda")
     U.umap_fuzzy_graph_device(n, k, di, dd, rows, cols, vals)
+    # the device fuzzy graph (smooth kNN, membership, union), timed on a second call
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    U.umap_fuzzy_graph_device(n, k, di, dd, rows, cols, vals)
+    e1.record()
     torch.cuda.synchronize()
+    build_input.fuzzy_graph_ms = e0.elapsed_time(e1)
     del di, dd
     a, b = U.umap_fit_ab(w.spread, w.min_dist)
     return ids, dist, rows, cols, vals, a, b
@@ -126,6 +133,7 @@ def gpu_steps(w, torch, U, coo, a, b, steps: int, warmup: int):
         log(f"step {s}: epochs {st['epochs_ms']:.2f} ms, init {st['init_ms']:.3f} ms, ingest {st['prep_ms']:.2f} ms, "
             f"{st['edge_updates']} edge updates")
     ok = bool(torch.isfinite(out).all().item())
+    gpu_steps.layout = out
     return stats, wall, ok
 
 
@@ -148,6 +156,60 @@ def async_mode(w, torch, U, coo, a, b, reps: int = 3) -> dict:
         "finite": finite,
         "note": "asynchronous in-place (Hogwild) updates, one launch per epoch; not bit-repeatable, quality "
                 "checked by the tests (trustworthiness within 0.01 of the oracle's)",
+    }
+
+
+def transform_measure(w, U, table: np.ndarray, a: float, b: float, n_new: int = 100_000, n_epochs: int = 100,
+                      reps: int = 3) -> dict:
+    """A transform of n_new new points against the fit's layout (frozen),
+    outside the timed steps: median device time of its epochs."""
+    from paper_2008_00325_amd import synth
+
+    r, c, v = synth.transform_graph(n_new, table.shape[0], w.k)
+    with U.umap_transform_create(n_new, table, r, c, v, a, b, n_epochs, w.neg_rate) as h:
+        runs = []
+        for s in range(reps):
+            U.umap_layout_run(h, 3000 + s)
+            runs.append(U.umap_layout_stats(h))
+        finite = bool(np.isfinite(U.umap_layout_get(h)).all())
+    ms = float(np.median([x["epochs_ms"] for x in runs]))
+    log(f"transform: {n_new} points, {n_epochs} epochs in {ms:.2f} ms")
+    return {
+        "n_new": n_new, "n_table": int(table.shape[0]), "k": w.k, "n_epochs": n_epochs,
+        "epochs_ms": ms,
+        "edge_updates_per_s": runs[-1]["edge_updates"] / (ms * 1e-3),
+        "table_ranges": runs[-1]["table_ranges"],
+        "finite": finite,
+        "note": "new points with k edges each into a +-64 window of the fit's layout, weights uniform on "
+                "[0.05, 1); only the new points move",
+    }
+
+
+def trustworthiness_measure(torch, U, n: int = 70_000, d: int = 784, k: int = 15, reps: int = 2) -> dict:
+    """The GPU trustworthiness on the 70,000 x 784 image-like points and a
+    random 2-D embedding: its dominant work is the n x n input distances as
+    fp32 MFMA tiles (2 n^2 d flops)."""
+    from paper_2008_00325_amd import synth
+
+    X, _ = synth.image_like(n, d)
+    Xg = torch.from_numpy(X).cuda()
+    Yg = torch.from_numpy(synth.embedding_state(n, 2, 1)).cuda()
+    U.umap_trustworthiness(Xg, Yg, k)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        U.umap_trustworthiness(Xg, Yg, k)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) / reps * 1e3
+    flops = 2.0 * n * n * d
+    tflops = flops / (ms * 1e-3) / 1e12
+    log(f"trustworthiness: n {n} x {d}, k {k}: {ms:.1f} ms, {tflops:.1f} TFLOP/s")
+    return {
+        "n": n, "d": d, "k": k, "ms": ms,
+        "roofline": {"bound": "mfma", "achieved": tflops, "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": tflops / FP32_MFMA_PEAK_TFLOPS,
+                     "note": "2 n^2 d flops of the input distances over the whole call (embedding kNN, "
+                             "thresholds and rank counting included), host-timed around the blocking call"},
     }
 
 
@@ -283,6 +345,8 @@ def main() -> int:
     achieved = bytes_epoch / (launch_ms * 1e-3) / 1e9
     traffic = profiled_traffic(w.name)
     async_stats = async_mode(w, torch, U, (rows, cols, vals), a, b)
+    transform_stats = transform_measure(w, U, gpu_steps.layout.cpu().numpy(), a, b)
+    trust_stats = trustworthiness_measure(torch, U)
     copy_gbps = copy_probe(torch, U)
     range_bytes = (w.n * w.dim * 4) // st["table_ranges"]
     table_pow2 = 1 << max(3, (range_bytes - 1).bit_length())
@@ -339,6 +403,9 @@ def main() -> int:
                     f"{w.n * w.dim * 4 / 1e6:.0f} MB table reaches {gather_full / 1e9:.0f} G/s",
         },
         "async_mode": async_stats,
+        "transform": transform_stats,
+        "trustworthiness": trust_stats,
+        "fuzzy_graph_ms": build_input.fuzzy_graph_ms,
         "hbm_copy_probe_GBps": copy_gbps,
         "gpu": gpu_name,
     }

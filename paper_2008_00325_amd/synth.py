@@ -188,3 +188,22 @@ def quality_sample(n: int, rows: int = 10_000, negatives: int = 64, seed: int = 
     r = np.sort(rng.choice(n, size=min(rows, n), replace=False)).astype(np.int64)
     neg = rng.integers(0, n, size=(r.size, negatives), dtype=np.int64)
     return r, neg
+
+
+def transform_graph(n_new: int, n_table: int, k: int = 15, seed: int = 6):
+    """Bipartite COO graph of n_new new points against n_table laid-out
+    vertices, for timing a transform: each new point picks an anchor row a
+    uniformly in [64, n_table - 65) and k distinct neighbours uniformly from
+    a - 64 .. a + 64, with weights uniform on [0.05, 1)."""
+    if n_table < 2 * WINDOW + 2:
+        raise ValueError("the table needs at least 130 rows")
+    rng = np.random.default_rng(seed)
+    anchor = rng.integers(WINDOW, n_table - WINDOW - 1, size=(n_new, 1))
+    rows = np.repeat(np.arange(n_new, dtype=np.int32), k)
+    cols = np.empty((n_new, k), dtype=np.int32)
+    for s in range(0, n_new, _BLOCK):
+        t = min(n_new, s + _BLOCK)
+        off = np.argsort(rng.random((t - s, 2 * WINDOW + 1)), axis=1)[:, :k] - WINDOW
+        cols[s:t] = (anchor[s:t] + off).astype(np.int32)
+    vals = rng.uniform(0.05, 1.0, size=rows.size).astype(np.float32)
+    return rows, cols.ravel(), vals
