@@ -789,18 +789,19 @@ int umap_trustworthiness(const float *X, int64_t n, int32_t d, const float *Y, i
         int ndev = 0;
         if (hipGetDeviceCount(&ndev) != hipSuccess || ndev < 1) return fail(UMAP_E_DEVICE, "no HIP device available");
         const size_t nk = (size_t)n * (size_t)k;
-        size_t bytes = need<float>(n) + need<int32_t>(nk) + need<float>(nk) + need<int64_t>(n) +
+        size_t bytes = need<float>(n) + need<int32_t>(nk) + need<float>(nk) + need<int32_t>(nk) + need<int64_t>(n) +
                        need<unsigned long long>(1) + need<unsigned>(1);
         UL_HIP(hipMallocAsync(&scratch, bytes, s));
         Carver cv{static_cast<char *>(scratch)};
         float *nx = cv.take<float>(n);
         int32_t *nbr = cv.take<int32_t>(nk);
         float *thr = cv.take<float>(nk);
+        int32_t *cnt = cv.take<int32_t>(nk);
         int64_t *pen = cv.take<int64_t>(n);
         unsigned long long *sum = cv.take<unsigned long long>(1);
         unsigned *flags = cv.take<unsigned>(1);
         UL_HIP(hipMemsetAsync(flags, 0, sizeof(unsigned), s));
-        UL_HIP(ul::launch_trustworthiness(X, n, d, Y, dim, k, nx, nbr, thr, pen, sum, flags, s));
+        UL_HIP(ul::launch_trustworthiness(X, n, d, Y, dim, k, nx, nbr, thr, cnt, pen, sum, flags, s));
         unsigned long long hsum = 0;
         unsigned hflags = 0;
         UL_HIP(hipMemcpyAsync(&hsum, sum, sizeof hsum, hipMemcpyDeviceToHost, s));

@@ -128,10 +128,11 @@ hipError_t launch_probe_gather(const void *table, int64_t entries, int64_t threa
                                hipStream_t s);
 
 // ---- trustworthiness (kernels_trust.hip) ----
-// Scratch: nx[n], nbr[n k], thr[n k], pen[n], sum[1], flags[1] (flags zeroed by the caller).
+// Scratch: nx[n], nbr[n k], thr[n k], cnt[n k], pen[n], sum[1], flags[1]
+// (flags zeroed by the caller).
 hipError_t launch_trustworthiness(const float *X, int64_t n, int32_t d, const float *Y, int32_t dim, int32_t k,
-                                  float *nx, int32_t *nbr, float *thr, int64_t *pen, unsigned long long *sum,
-                                  unsigned *flags, hipStream_t s);
+                                  float *nx, int32_t *nbr, float *thr, int32_t *cnt, int64_t *pen,
+                                  unsigned long long *sum, unsigned *flags, hipStream_t s);
 
 // ---- fuzzy graph (kernels_graph.hip) ----
 hipError_t launch_fuzzy_graph(int64_t n, int32_t k, const int32_t *ids, const float *dists, int32_t *rows,

@@ -13,20 +13,18 @@
 //  2. k_tw_embed_knn: one wavefront per point, a brute-force scan of the
 //     embedding keeping the k best (distance, index) pairs sorted across lanes.
 //  3. k_tw_thresholds: input distance from i to each embedding neighbour.
-//  4. k_tw_rank: the input distances of a block of 64 points to all n points as
-//     fp32 MFMA tiles (v_mfma_f32_16x16x4f32), turned into distances in
-//     registers and compared with each point's neighbour thresholds: only the
-//     counts r(i, j) - 1 leave the chip, never the n x n distances.
-//  5. k_tw_penalty: per-point penalty sum, then one fixed-order reduction.
+//  4. k_tw_rank: the input distances of blocks of 128 points to tiles of
+//     columns as fp32 MFMA tiles (v_mfma_f32_16x16x4f32), turned into
+//     distances in registers and compared with each point's neighbour
+//     thresholds: only the counts r(i, j) - 1 leave the chip, never the n x n
+//     distances.
+//  5. k_tw_penalty: per-point penalty sum; k_tw_sum: one fixed-order reduction.
 #include "internal.hpp"
 
 namespace ul {
 
 typedef float v4f __attribute__((ext_vector_type(4)));
 
-constexpr int kTwRows = 64;    // points per rank block (4 waves x 16)
-constexpr int kTwCols = 64;    // column tile (4 MFMA tiles of 16)
-constexpr int kTwChunk = 16;   // input features per LDS chunk (4 MFMA k-steps)
 
 __global__ __launch_bounds__(256) void k_tw_norms(const float *__restrict__ X, int64_t n, int32_t d,
                                                   float *__restrict__ nx)
@@ -124,24 +122,64 @@ __global__ __launch_bounds__(256) void k_tw_thresholds(const float *__restrict__
     thr[t] = nx[i] + nx[j] - 2.0f * dot;
 }
 
-// Block: 64 points (rows) x all n points (columns), 4 waves of 16 rows.
-// Lane l of a wave owns row (wave base + l % 16) and, in each of the 4 column
-// sub-tiles, the 4 columns 4 * (l / 16) + 0..3 of the MFMA result layout.
-template <int KMAX>
-__global__ __launch_bounds__(256) void k_tw_rank(const float *__restrict__ X, int64_t n, int32_t d, int32_t k,
-                                                 const float *__restrict__ nx, const int32_t *__restrict__ nbr,
-                                                 const float *__restrict__ thr, int64_t *__restrict__ pen)
+// Input distances of a block of kRkRows points (rows) to a range of column
+// tiles of CT x 16 points, as fp32 MFMA tiles (v_mfma_f32_16x16x4f32), turned
+// into distances in registers and compared with each row's k thresholds.
+//
+//  * 8 waves; wave w owns rows 16 w .. 16 w + 15 of the block: lane l holds
+//    row l % 16 and, in each of the CT column tiles of 16, the four columns
+//    4 (l / 16) + 0..3 of the MFMA result layout.
+//  * The features are taken 16 at a time, double buffered in LDS
+//    ([point][feature], padded to 20 floats so that a lane's 16-byte read of
+//    four features is free of bank conflicts), the next chunk's global loads
+//    in flight while the current one is multiplied.  Lane group g = l / 16
+//    supplies feature 4 g + j at MFMA step j, so both operands of a lane come
+//    from one 16-byte LDS read.
+//  * Column splits (blockIdx.y) keep enough blocks in flight; each block adds
+//    its rows' partial counts to cnt[row * k + s] with integer atomics (exact,
+//    order-free).
+constexpr int kRkRows = 128;
+constexpr int kRkChunk = 16;
+constexpr int kRkPad = 20;
+
+__device__ __forceinline__ float4 load_features(const float *__restrict__ X, int64_t p, int32_t q, int64_t n,
+                                                int32_t d, bool vec)
 {
-    __shared__ float s_rows[kTwChunk][kTwRows];   // [feature][row]
-    __shared__ float s_cols[kTwChunk][kTwCols];   // [feature][column]
+    float4 v = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    if (p >= n) return v;
+    const float *x = X + p * d + q;
+    if (vec) {
+        if (q < d) v = *reinterpret_cast<const float4 *>(x);
+    } else {
+        if (q < d) v.x = x[0];
+        if (q + 1 < d) v.y = x[1];
+        if (q + 2 < d) v.z = x[2];
+        if (q + 3 < d) v.w = x[3];
+    }
+    return v;
+}
+
+template <int KMAX, int CT>
+__global__ __launch_bounds__(512) void k_tw_rank(const float *__restrict__ X, int64_t n, int32_t d, int32_t k,
+                                                 const float *__restrict__ nx, const int32_t *__restrict__ nbr,
+                                                 const float *__restrict__ thr, int64_t tiles_per_split,
+                                                 int32_t *__restrict__ cnt_out)
+{
+    constexpr int COLS = 16 * CT;
+    __shared__ __align__(16) float s_rows[2][kRkRows * kRkPad];
+    __shared__ __align__(16) float s_cols[2][COLS * kRkPad];
+    __shared__ float s_nx[COLS];
 
     const int tid = threadIdx.x;
     const int lane = tid % kWave;
     const int wv = tid / kWave;
-    const int64_t row0 = (int64_t)blockIdx.x * kTwRows;
-    const int rloc = wv * 16 + (lane & 15);
+    const int g = lane / 16;
+    const int li = lane % 16;
+    const int64_t row0 = (int64_t)blockIdx.x * kRkRows;
+    const int rloc = wv * 16 + li;
     const int64_t row = row0 + rloc;
     const bool row_ok = row < n;
+    const bool vec = (d % 4) == 0 && (reinterpret_cast<uintptr_t>(X) & 15) == 0;   // 16-byte loads
 
     float th[KMAX];
     int32_t nb[KMAX];
@@ -155,61 +193,115 @@ __global__ __launch_bounds__(256) void k_tw_rank(const float *__restrict__ X, in
     }
     const float nrow = row_ok ? nx[row] : 0.0f;
 
-    // staging: thread tid loads feature (tid % 16) of point (tid / 16) + 16 m
-    const int lq = tid % kTwChunk;
-    const int lp = tid / kTwChunk;   // 0..15
-    for (int64_t col0 = 0; col0 < n; col0 += kTwCols) {
-        v4f acc[4];
+    // staging: thread t moves features 4 (t % 4) .. +3 of point t / 4
+    const int sp = tid / 4;
+    const int sq = 4 * (tid % 4);
+    const bool stage_col = sp < COLS;
+    const int64_t n_tiles = (n + COLS - 1) / COLS;
+    const int64_t t0 = (int64_t)blockIdx.y * tiles_per_split;
+    const int64_t t1 = t0 + tiles_per_split < n_tiles ? t0 + tiles_per_split : n_tiles;
+
+    for (int64_t tile = t0; tile < t1; ++tile) {
+        const int64_t col0 = tile * COLS;
+        if (tid < COLS) s_nx[tid] = col0 + tid < n ? nx[col0 + tid] : 0.0f;
+        v4f acc[CT];
 #pragma unroll
-        for (int t = 0; t < 4; ++t) acc[t] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
-        for (int32_t q0 = 0; q0 < d; q0 += kTwChunk) {
-            const int32_t q = q0 + lq;
+        for (int t = 0; t < CT; ++t) acc[t] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
+
+        float4 rv = load_features(X, row0 + sp, sq, n, d, vec);
+        float4 cv = stage_col ? load_features(X, col0 + sp, sq, n, d, vec) : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        *reinterpret_cast<float4 *>(&s_rows[0][sp * kRkPad + sq]) = rv;
+        if (stage_col) *reinterpret_cast<float4 *>(&s_cols[0][sp * kRkPad + sq]) = cv;
+        __syncthreads();
+        int buf = 0;
+        for (int32_t q0 = 0; q0 < d; q0 += kRkChunk) {
+            const bool more = q0 + kRkChunk < d;
+            if (more) {
+                rv = load_features(X, row0 + sp, q0 + kRkChunk + sq, n, d, vec);
+                if (stage_col) cv = load_features(X, col0 + sp, q0 + kRkChunk + sq, n, d, vec);
+            }
+            const float4 bq = *reinterpret_cast<const float4 *>(&s_rows[buf][rloc * kRkPad + 4 * g]);
+            float4 aq[CT];
 #pragma unroll
-            for (int m = 0; m < 4; ++m) {
-                const int p = lp + 16 * m;
-                const int64_t r = row0 + p;
-                const int64_t c = col0 + p;
-                s_rows[lq][p] = (q < d && r < n) ? X[r * d + q] : 0.0f;
-                s_cols[lq][p] = (q < d && c < n) ? X[c * d + q] : 0.0f;
+            for (int t = 0; t < CT; ++t)
+                aq[t] = *reinterpret_cast<const float4 *>(&s_cols[buf][(t * 16 + li) * kRkPad + 4 * g]);
+#pragma unroll
+            for (int t = 0; t < CT; ++t) {
+                acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(aq[t].x, bq.x, acc[t], 0, 0, 0);
+                acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(aq[t].y, bq.y, acc[t], 0, 0, 0);
+                acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(aq[t].z, bq.z, acc[t], 0, 0, 0);
+                acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(aq[t].w, bq.w, acc[t], 0, 0, 0);
+            }
+            if (more) {
+                *reinterpret_cast<float4 *>(&s_rows[buf ^ 1][sp * kRkPad + sq]) = rv;
+                if (stage_col) *reinterpret_cast<float4 *>(&s_cols[buf ^ 1][sp * kRkPad + sq]) = cv;
             }
             __syncthreads();
+            buf ^= 1;
+        }
+        if (row_ok) {
 #pragma unroll
-            for (int ks = 0; ks < kTwChunk; ks += 4) {
-                const float b = s_rows[ks + lane / 16][wv * 16 + (lane & 15)];
+            for (int t = 0; t < CT; ++t) {
 #pragma unroll
-                for (int t = 0; t < 4; ++t) {
-                    const float a = s_cols[ks + lane / 16][t * 16 + (lane & 15)];
-                    acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc[t], 0, 0, 0);
+                for (int e = 0; e < 4; ++e) {
+                    const int cl = t * 16 + 4 * g + e;
+                    const int64_t c = col0 + cl;
+                    if (c >= n || c == row) continue;
+                    const float dist = nrow + s_nx[cl] - 2.0f * acc[t][e];
+                    const int32_t ci = (int32_t)c;
+#pragma unroll
+                    for (int s = 0; s < KMAX; ++s)
+                        cnt[s] += (ci != nb[s] && pair_less(dist, ci, th[s], nb[s])) ? 1 : 0;
                 }
             }
-            __syncthreads();
         }
-        if (!row_ok) continue;
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int64_t c = col0 + t * 16 + 4 * (lane / 16) + e;
-                if (c >= n || c == row) continue;
-                const float dist = nrow + nx[c] - 2.0f * acc[t][e];
-                const int32_t ci = (int32_t)c;
-#pragma unroll
-                for (int s = 0; s < KMAX; ++s)
-                    cnt[s] += (ci != nb[s] && pair_less(dist, ci, th[s], nb[s])) ? 1 : 0;
-            }
-        }
+        __syncthreads();   // s_nx and the buffers are refilled for the next tile
     }
     // the four lanes of a row (l, l + 16, l + 32, l + 48) hold disjoint columns
-    int64_t p = 0;
 #pragma unroll
     for (int s = 0; s < KMAX; ++s) {
         int32_t c = cnt[s];
         c += __shfl_xor(c, 16);
         c += __shfl_xor(c, 32);
-        const int64_t rank = (int64_t)c + 1;
-        if (s < k && rank > k) p += rank - k;
+        if (row_ok && g == 0 && s < k && c != 0) atomicAdd(&cnt_out[row * k + s], c);
     }
-    if (row_ok && lane < 16) pen[row] = p;
+}
+
+// pen[i] = sum_s max(0, r(i, nbr_s) - k), r = 1 + the count of points before
+// the neighbour.
+__global__ __launch_bounds__(256) void k_tw_penalty(const int32_t *__restrict__ cnt, int64_t n, int32_t k,
+                                                    int64_t *__restrict__ pen)
+{
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= n) return;
+    int64_t p = 0;
+    for (int32_t s = 0; s < k; ++s) {
+        const int64_t rank = (int64_t)cnt[i * k + s] + 1;
+        if (rank > k) p += rank - k;
+    }
+    pen[i] = p;
+}
+
+__global__ __launch_bounds__(256) void k_tw_zero(int32_t *__restrict__ p, int64_t count)
+{
+    const int64_t stride = (int64_t)gridDim.x * 256;
+    for (int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x; t < count; t += stride) p[t] = 0;
+}
+
+template <int KMAX, int CT>
+static void launch_rank(const float *X, int64_t n, int32_t d, int32_t k, const float *nx, const int32_t *nbr,
+                        const float *thr, int32_t *cnt, hipStream_t s)
+{
+    const int64_t row_blocks = (n + kRkRows - 1) / kRkRows;
+    const int64_t n_tiles = (n + 16 * CT - 1) / (16 * CT);
+    // at least ~2048 blocks when the columns allow it
+    int64_t splits = (2048 + row_blocks - 1) / row_blocks;
+    if (splits > n_tiles) splits = n_tiles;
+    if (splits < 1) splits = 1;
+    const int64_t per_split = (n_tiles + splits - 1) / splits;
+    splits = (n_tiles + per_split - 1) / per_split;
+    hipLaunchKernelGGL((k_tw_rank<KMAX, CT>), dim3((unsigned)row_blocks, (unsigned)splits), dim3(512), 0, s, X, n,
+                       d, k, nx, nbr, thr, per_split, cnt);
 }
 
 // Sum of pen[0..n) in a fixed order: one block, strided partial sums, then a
@@ -238,8 +330,8 @@ static hipError_t launch_knn_dim(const float *Y, int64_t n, int32_t k, int32_t *
 }
 
 hipError_t launch_trustworthiness(const float *X, int64_t n, int32_t d, const float *Y, int32_t dim, int32_t k,
-                                  float *nx, int32_t *nbr, float *thr, int64_t *pen, unsigned long long *sum,
-                                  unsigned *flags, hipStream_t s)
+                                  float *nx, int32_t *nbr, float *thr, int32_t *cnt, int64_t *pen,
+                                  unsigned long long *sum, unsigned *flags, hipStream_t s)
 {
     hipLaunchKernelGGL(k_tw_norms, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, X, n, d, nx);
     hipError_t e = hipSuccess;
@@ -254,13 +346,16 @@ hipError_t launch_trustworthiness(const float *X, int64_t n, int32_t d, const fl
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k_tw_thresholds, dim3((unsigned)((n * k + 255) / 256)), dim3(256), 0, s, X, n, d, k, nx, nbr,
                        thr, flags);
-    const unsigned blocks = (unsigned)((n + kTwRows - 1) / kTwRows);
+    const int64_t nk = n * k;
+    hipLaunchKernelGGL(k_tw_zero, dim3((unsigned)((nk + 255) / 256 < 4096 ? (nk + 255) / 256 : 4096)), dim3(256), 0,
+                       s, cnt, nk);
     if (k <= 16)
-        hipLaunchKernelGGL((k_tw_rank<16>), dim3(blocks), dim3(256), 0, s, X, n, d, k, nx, nbr, thr, pen);
+        launch_rank<16, 8>(X, n, d, k, nx, nbr, thr, cnt, s);
     else if (k <= 32)
-        hipLaunchKernelGGL((k_tw_rank<32>), dim3(blocks), dim3(256), 0, s, X, n, d, k, nx, nbr, thr, pen);
+        launch_rank<32, 4>(X, n, d, k, nx, nbr, thr, cnt, s);
     else
-        hipLaunchKernelGGL((k_tw_rank<64>), dim3(blocks), dim3(256), 0, s, X, n, d, k, nx, nbr, thr, pen);
+        launch_rank<64, 2>(X, n, d, k, nx, nbr, thr, cnt, s);
+    hipLaunchKernelGGL(k_tw_penalty, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, cnt, n, k, pen);
     hipLaunchKernelGGL(k_tw_sum, dim3(1), dim3(256), 0, s, pen, n, sum);
     return hipGetLastError();
 }
