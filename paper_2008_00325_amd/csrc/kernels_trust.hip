@@ -129,18 +129,17 @@ __global__ __launch_bounds__(256) void k_tw_thresholds(const float *__restrict__
 //  * 8 waves; wave w owns rows 16 w .. 16 w + 15 of the block: lane l holds
 //    row l % 16 and, in each of the CT column tiles of 16, the four columns
 //    4 (l / 16) + 0..3 of the MFMA result layout.
-//  * The features are taken 16 at a time, double buffered in LDS
-//    ([point][feature], padded to 20 floats so that a lane's 16-byte read of
-//    four features is free of bank conflicts), the next chunk's global loads
-//    in flight while the current one is multiplied.  Lane group g = l / 16
-//    supplies feature 4 g + j at MFMA step j, so both operands of a lane come
-//    from one 16-byte LDS read.
+//  * The features are taken CH (16 or 32) at a time, double buffered in LDS
+//    ([point][feature], padded to CH + 4 floats so that a lane's 16-byte reads
+//    are free of bank conflicts), the next chunk's global loads in flight while
+//    the current one is multiplied.  Lane group g = l / 16 supplies features
+//    g CH/4 .. (g + 1) CH/4 - 1, one per MFMA step, so each operand of a lane
+//    comes from CH/16 16-byte LDS reads.
 //  * Column splits (blockIdx.y) keep enough blocks in flight; each block adds
 //    its rows' partial counts to cnt[row * k + s] with integer atomics (exact,
 //    order-free).
 constexpr int kRkRows = 128;
-constexpr int kRkChunk = 16;
-constexpr int kRkPad = 20;
+constexpr int kRankChunk = 16;   // features per LDS stage
 
 __device__ __forceinline__ float4 load_features(const float *__restrict__ X, int64_t p, int32_t q, int64_t n,
                                                 int32_t d, bool vec)
@@ -159,15 +158,20 @@ __device__ __forceinline__ float4 load_features(const float *__restrict__ X, int
     return v;
 }
 
-template <int KMAX, int CT>
+template <int KMAX, int CT, int CH>
 __global__ __launch_bounds__(512) void k_tw_rank(const float *__restrict__ X, int64_t n, int32_t d, int32_t k,
                                                  const float *__restrict__ nx, const int32_t *__restrict__ nbr,
                                                  const float *__restrict__ thr, int64_t tiles_per_split,
                                                  int32_t *__restrict__ cnt_out)
 {
     constexpr int COLS = 16 * CT;
-    __shared__ __align__(16) float s_rows[2][kRkRows * kRkPad];
-    __shared__ __align__(16) float s_cols[2][COLS * kRkPad];
+    constexpr int PAD = CH + 4;        // floats per staged point
+    constexpr int QUADS = CH / 4;      // float4 per staged point
+    constexpr int NV = QUADS / 4;      // float4 a thread stages per operand (512 threads, 128 points)
+    constexpr int GQ = CH / 16;        // float4 per lane group per operand
+    static_assert(CH == 16 || CH == 32, "chunk of 16 or 32 features");
+    __shared__ __align__(16) float s_rows[2][kRkRows * PAD];
+    __shared__ __align__(16) float s_cols[2][COLS * PAD];
     __shared__ float s_nx[COLS];
 
     const int tid = threadIdx.x;
@@ -193,10 +197,14 @@ __global__ __launch_bounds__(512) void k_tw_rank(const float *__restrict__ X, in
     }
     const float nrow = row_ok ? nx[row] : 0.0f;
 
-    // staging: thread t moves features 4 (t % 4) .. +3 of point t / 4
-    const int sp = tid / 4;
-    const int sq = 4 * (tid % 4);
-    const bool stage_col = sp < COLS;
+    // staging: float4 number f = tid + 512 v (v < NV) is features
+    // 4 (f % QUADS) .. +3 of point f / QUADS
+    int sp[NV], sq[NV];
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+        sp[v] = (tid + 512 * v) / QUADS;
+        sq[v] = 4 * ((tid + 512 * v) % QUADS);
+    }
     const int64_t n_tiles = (n + COLS - 1) / COLS;
     const int64_t t0 = (int64_t)blockIdx.y * tiles_per_split;
     const int64_t t1 = t0 + tiles_per_split < n_tiles ? t0 + tiles_per_split : n_tiles;
@@ -208,34 +216,46 @@ __global__ __launch_bounds__(512) void k_tw_rank(const float *__restrict__ X, in
 #pragma unroll
         for (int t = 0; t < CT; ++t) acc[t] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
 
-        float4 rv = load_features(X, row0 + sp, sq, n, d, vec);
-        float4 cv = stage_col ? load_features(X, col0 + sp, sq, n, d, vec) : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-        *reinterpret_cast<float4 *>(&s_rows[0][sp * kRkPad + sq]) = rv;
-        if (stage_col) *reinterpret_cast<float4 *>(&s_cols[0][sp * kRkPad + sq]) = cv;
+        float4 rv[NV], cv[NV];
+        auto fetch = [&](int32_t q0) __attribute__((always_inline)) {
+#pragma unroll
+            for (int v = 0; v < NV; ++v) {
+                rv[v] = load_features(X, row0 + sp[v], q0 + sq[v], n, d, vec);
+                cv[v] = sp[v] < COLS ? load_features(X, col0 + sp[v], q0 + sq[v], n, d, vec)
+                                     : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            }
+        };
+        auto stash = [&](int b) __attribute__((always_inline)) {
+#pragma unroll
+            for (int v = 0; v < NV; ++v) {
+                *reinterpret_cast<float4 *>(&s_rows[b][sp[v] * PAD + sq[v]]) = rv[v];
+                if (sp[v] < COLS) *reinterpret_cast<float4 *>(&s_cols[b][sp[v] * PAD + sq[v]]) = cv[v];
+            }
+        };
+        fetch(0);
+        stash(0);
         __syncthreads();
         int buf = 0;
-        for (int32_t q0 = 0; q0 < d; q0 += kRkChunk) {
-            const bool more = q0 + kRkChunk < d;
-            if (more) {
-                rv = load_features(X, row0 + sp, q0 + kRkChunk + sq, n, d, vec);
-                if (stage_col) cv = load_features(X, col0 + sp, q0 + kRkChunk + sq, n, d, vec);
-            }
-            const float4 bq = *reinterpret_cast<const float4 *>(&s_rows[buf][rloc * kRkPad + 4 * g]);
-            float4 aq[CT];
+        for (int32_t q0 = 0; q0 < d; q0 += CH) {
+            const bool more = q0 + CH < d;
+            if (more) fetch(q0 + CH);
 #pragma unroll
-            for (int t = 0; t < CT; ++t)
-                aq[t] = *reinterpret_cast<const float4 *>(&s_cols[buf][(t * 16 + li) * kRkPad + 4 * g]);
+            for (int gq = 0; gq < GQ; ++gq) {
+                const int f = g * (CH / 4) + 4 * gq;   // this lane group's features f .. f + 3
+                const float4 bq = *reinterpret_cast<const float4 *>(&s_rows[buf][rloc * PAD + f]);
+                float4 aq[CT];
 #pragma unroll
-            for (int t = 0; t < CT; ++t) {
-                acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(aq[t].x, bq.x, acc[t], 0, 0, 0);
-                acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(aq[t].y, bq.y, acc[t], 0, 0, 0);
-                acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(aq[t].z, bq.z, acc[t], 0, 0, 0);
-                acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(aq[t].w, bq.w, acc[t], 0, 0, 0);
+                for (int t = 0; t < CT; ++t)
+                    aq[t] = *reinterpret_cast<const float4 *>(&s_cols[buf][(t * 16 + li) * PAD + f]);
+#pragma unroll
+                for (int t = 0; t < CT; ++t) {
+                    acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(aq[t].x, bq.x, acc[t], 0, 0, 0);
+                    acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(aq[t].y, bq.y, acc[t], 0, 0, 0);
+                    acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(aq[t].z, bq.z, acc[t], 0, 0, 0);
+                    acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(aq[t].w, bq.w, acc[t], 0, 0, 0);
+                }
             }
-            if (more) {
-                *reinterpret_cast<float4 *>(&s_rows[buf ^ 1][sp * kRkPad + sq]) = rv;
-                if (stage_col) *reinterpret_cast<float4 *>(&s_cols[buf ^ 1][sp * kRkPad + sq]) = cv;
-            }
+            if (more) stash(buf ^ 1);
             __syncthreads();
             buf ^= 1;
         }
@@ -288,7 +308,7 @@ __global__ __launch_bounds__(256) void k_tw_zero(int32_t *__restrict__ p, int64_
     for (int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x; t < count; t += stride) p[t] = 0;
 }
 
-template <int KMAX, int CT>
+template <int KMAX, int CT, int CH = kRankChunk>
 static void launch_rank(const float *X, int64_t n, int32_t d, int32_t k, const float *nx, const int32_t *nbr,
                         const float *thr, int32_t *cnt, hipStream_t s)
 {
@@ -300,7 +320,7 @@ static void launch_rank(const float *X, int64_t n, int32_t d, int32_t k, const f
     if (splits < 1) splits = 1;
     const int64_t per_split = (n_tiles + splits - 1) / splits;
     splits = (n_tiles + per_split - 1) / per_split;
-    hipLaunchKernelGGL((k_tw_rank<KMAX, CT>), dim3((unsigned)row_blocks, (unsigned)splits), dim3(512), 0, s, X, n,
+    hipLaunchKernelGGL((k_tw_rank<KMAX, CT, CH>), dim3((unsigned)row_blocks, (unsigned)splits), dim3(512), 0, s, X, n,
                        d, k, nx, nbr, thr, per_split, cnt);
 }
 
