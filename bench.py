@@ -311,6 +311,9 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="window1m")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the asynchronous-mode, transform and trustworthiness figures (profiling runs of "
+                         "the fit's kernels)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (the layout is measured on a single MI355X); got --gpus {args.gpus}",
@@ -344,9 +347,11 @@ def main() -> int:
     launch_ms = epochs_ms / n_epochs
     achieved = bytes_epoch / (launch_ms * 1e-3) / 1e9
     traffic = profiled_traffic(w.name)
-    async_stats = async_mode(w, torch, U, (rows, cols, vals), a, b)
-    transform_stats = transform_measure(w, U, gpu_steps.layout.cpu().numpy(), a, b)
-    trust_stats = trustworthiness_measure(torch, U)
+    async_stats = transform_stats = trust_stats = None
+    if not args.no_extras:
+        async_stats = async_mode(w, torch, U, (rows, cols, vals), a, b)
+        transform_stats = transform_measure(w, U, gpu_steps.layout.cpu().numpy(), a, b)
+        trust_stats = trustworthiness_measure(torch, U)
     copy_gbps = copy_probe(torch, U)
     range_bytes = (w.n * w.dim * 4) // st["table_ranges"]
     table_pow2 = 1 << max(3, (range_bytes - 1).bit_length())
@@ -402,9 +407,8 @@ def main() -> int:
                     f"vertex-table range, the slice one repulsion launch gathers from); the probe on the whole "
                     f"{w.n * w.dim * 4 / 1e6:.0f} MB table reaches {gather_full / 1e9:.0f} G/s",
         },
-        "async_mode": async_stats,
-        "transform": transform_stats,
-        "trustworthiness": trust_stats,
+        **({} if args.no_extras else {"async_mode": async_stats, "transform": transform_stats,
+                                       "trustworthiness": trust_stats}),
         "fuzzy_graph_ms": build_input.fuzzy_graph_ms,
         "hbm_copy_probe_GBps": copy_gbps,
         "gpu": gpu_name,
