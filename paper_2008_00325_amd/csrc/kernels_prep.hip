@@ -75,16 +75,45 @@ __global__ __launch_bounds__(256) void k_check_max(const int32_t *__restrict__ r
     }
 }
 
+// Slot of the calling lane in the counter ctr[key], with one atomic add per
+// run of consecutive lanes that hold the same key (inactive lanes end a run):
+// the counter's old value plus the lane's rank in its run.  Kernel-built
+// graphs list a row's entries together, so runs are long.  Every lane of the
+// wave must call it.
+__device__ __forceinline__ int32_t run_atomic_add(int32_t *ctr, int32_t key, bool active)
+{
+    const int lane = (int)lane_id();
+    const int32_t prev = __shfl_up(key, 1);
+    const unsigned long long act = __ballot(active);
+    const bool prev_act = lane > 0 && ((act >> (lane - 1)) & 1ull);
+    const bool head = active && !(prev_act && prev == key);
+    const unsigned long long heads = __ballot(head);
+    const unsigned long long le = (2ull << lane) - 1ull;   // lanes 0 .. lane
+    int32_t base = 0;
+    if (head) {
+        const unsigned long long above = (heads | ~act) & ~le;
+        const int end = above ? __builtin_ctzll(above) : 64;
+        base = atomicAdd(&ctr[key], end - lane);
+    }
+    const unsigned long long hm = heads & le;
+    const int h = hm ? 63 - __builtin_clzll(hm) : lane;
+    return __shfl(base, h) + lane - h;
+}
+
 __global__ __launch_bounds__(256) void k_count(const int32_t *__restrict__ rows, const int32_t *__restrict__ cols,
                                                const float *__restrict__ vals, int64_t nnz, IngestShape sh,
                                                int32_t n_epochs, const PrepScalars *S, int32_t *__restrict__ deg)
 {
     const float thresh = keep_threshold(S, n_epochs);
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < nnz; t += stride) {
-        int32_t r = rows[t], c = cols[t];
-        float v = vals[t];
-        if (candidate(r, c, v, sh) && v >= thresh) atomicAdd(&deg[r], 1);
+    // wave-uniform trip count: run_atomic_add needs the whole wave
+    for (int64_t t0 = (int64_t)blockIdx.x * blockDim.x + (threadIdx.x & ~63u); t0 < nnz; t0 += stride) {
+        const int64_t t = t0 + (threadIdx.x & 63u);
+        const bool in = t < nnz;
+        const int32_t r = in ? rows[t] : 0, c = in ? cols[t] : 0;
+        const float v = in ? vals[t] : 0.0f;
+        const bool keep = in && candidate(r, c, v, sh) && v >= thresh;
+        run_atomic_add(deg, r, keep);
     }
 }
 
@@ -177,11 +206,15 @@ __global__ __launch_bounds__(256) void k_scatter(const int32_t *__restrict__ row
 {
     const float thresh = keep_threshold(S, n_epochs);
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < nnz; t += stride) {
-        int32_t r = rows[t], c = cols[t];
-        float v = vals[t];
-        if (candidate(r, c, v, sh) && v >= thresh) {
-            int64_t p = row_ptr[r] + atomicAdd(&cursor[r], 1);
+    for (int64_t t0 = (int64_t)blockIdx.x * blockDim.x + (threadIdx.x & ~63u); t0 < nnz; t0 += stride) {
+        const int64_t t = t0 + (threadIdx.x & 63u);
+        const bool in = t < nnz;
+        const int32_t r = in ? rows[t] : 0, c = in ? cols[t] : 0;
+        const float v = in ? vals[t] : 0.0f;
+        const bool keep = in && candidate(r, c, v, sh) && v >= thresh;
+        const int32_t slot = run_atomic_add(cursor, r, keep);
+        if (keep) {
+            const int64_t p = row_ptr[r] + slot;
             trow[p] = r;
             tcol[p] = c;
             tval[p] = v;
