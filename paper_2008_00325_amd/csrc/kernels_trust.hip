@@ -370,7 +370,7 @@ hipError_t launch_trustworthiness(const float *X, int64_t n, int32_t d, const fl
     hipLaunchKernelGGL(k_tw_zero, dim3((unsigned)((nk + 255) / 256 < 4096 ? (nk + 255) / 256 : 4096)), dim3(256), 0,
                        s, cnt, nk);
     if (k <= 16)
-        launch_rank<16, 8>(X, n, d, k, nx, nbr, thr, cnt, s);
+        launch_rank<16, 4>(X, n, d, k, nx, nbr, thr, cnt, s);
     else if (k <= 32)
         launch_rank<32, 4>(X, n, d, k, nx, nbr, thr, cnt, s);
     else
