@@ -193,7 +193,7 @@ int create_common(umap_layout **out, int64_t n, int32_t dim, const int32_t *rows
 
         // persistent arena; the wave count is bounded with nnz (kept <= nnz)
         const int wgt = ul::row_weight(dim);
-        const int64_t max_waves = (nnz + (int64_t)wgt * n) / ul::kWaveCost + 2;
+        const int64_t max_waves = ul::max_wave_count(nnz + (int64_t)wgt * n);
         const size_t nd = (size_t)n * (size_t)dim;
         const int64_t count_stride =
             ul::count_slots(1, n, 0) > max_waves ? ul::count_slots(1, n, 0) : max_waves;
@@ -305,9 +305,12 @@ int create_common(umap_layout **out, int64_t n, int32_t dim, const int32_t *rows
         h->nnz = kept;
         h->max_degree = S.max_degree;
         memcpy(&h->w_max, &S.wmax_bits, sizeof(float));
-        h->n_waves = (kept + (int64_t)wgt * n + ul::kWaveCost - 1) / ul::kWaveCost;
+        const int64_t units = kept + (int64_t)wgt * n;
+        const int64_t cost = ul::wave_cost(units);
+        h->n_waves = (units + cost - 1) / cost;
         if (h->n_waves < 1) h->n_waves = 1;
-        UL_HIP(ul::launch_partition(h->row_ptr, n, dim, h->part, h->n_waves, h->head, stream));
+        if (h->n_waves > max_waves) throw HipFailure{hipErrorInvalidValue, "wave count exceeds the arena"};
+        UL_HIP(ul::launch_partition(h->row_ptr, n, dim, cost, h->part, h->n_waves, h->head, stream));
         float ms = 0;
         UL_HIP(hipEventElapsedTime(&ms, h->ev[0], h->ev[1]));
         h->st.prep_ms = ms;

@@ -27,14 +27,31 @@ struct PrepScalars {
     int pad;
 };
 
-// Work split of the wavefront epoch kernel: wave w owns the whole rows
-// [part[w], part[w+1]), chosen so that consecutive waves cover about
-// kWaveCost units of (edges + row_weight * rows).  The row weight bounds the
-// rows of a wave (and so its LDS accumulator) by rows_cap; long waves amortise
-// the per-wave set-up and commit.
+// Work split of the wavefront epoch kernels: wave w owns the whole rows
+// [part[w], part[w+1]), chosen so that consecutive waves cover about C units
+// of (edges + row_weight * rows), C = wave_cost(total units) <= kWaveCost.  The
+// row weight bounds the rows of a wave (and so its LDS accumulator) by
+// rows_cap; long waves amortise the per-wave set-up and commit, and C shrinks
+// (by halves, down to kMinWaveCost) until a graph gives at least
+// kTargetWaves waves, so that small graphs still fill the chip.
 constexpr int kWaveCost = 8192;
+constexpr int kMinWaveCost = 256;
+constexpr int64_t kTargetWaves = 4096;
 __host__ __device__ constexpr int row_weight(int dim) { return 32 * (dim > 2 ? dim : 2); }
 __host__ __device__ constexpr int rows_cap(int dim) { return kWaveCost / row_weight(dim) + 1; }
+inline int64_t wave_cost(int64_t total_units)
+{
+    int64_t c = kWaveCost;
+    while (c > kMinWaveCost && total_units / c < kTargetWaves) c >>= 1;
+    return c;
+}
+// Most waves any graph of at most `total_units` gets (wave_cost grows with the
+// total, so a smaller total never needs more than 2 kTargetWaves).
+inline int64_t max_wave_count(int64_t total_units)
+{
+    const int64_t big = total_units / kWaveCost;
+    return (big > 2 * kTargetWaves ? big : 2 * kTargetWaves) + 2;
+}
 
 // ---- ingest (kernels_prep.hip) ----
 struct PrepBuffers {
@@ -65,8 +82,8 @@ struct PrepBuffers {
 
 int64_t scan_blocks(int64_t n);
 hipError_t launch_prep(const PrepBuffers &B, hipStream_t s);
-hipError_t launch_partition(const int64_t *row_ptr, int64_t n, int32_t dim, int32_t *part, int64_t n_waves,
-                            uint8_t *head, hipStream_t s);
+hipError_t launch_partition(const int64_t *row_ptr, int64_t n, int32_t dim, int64_t cost, int32_t *part,
+                            int64_t n_waves, uint8_t *head, hipStream_t s);
 hipError_t launch_zero_u64(unsigned long long *p, int64_t count, hipStream_t s);
 
 // ---- layout (kernels_layout.hip) ----

@@ -310,12 +310,12 @@ hipError_t launch_prep(const PrepBuffers &B, hipStream_t s)
     return hipGetLastError();
 }
 
-// part[w] = first row r with row_ptr[r] + wgt * r >= w * kWaveCost, for
-// w < n_waves; part[n_waves] = n.  A wave then holds at most rows_cap(dim)
-// rows (cost rises by >= wgt per row) and about kWaveCost edges unless its
-// last row alone is longer.
-__global__ void k_partition(const int64_t *__restrict__ row_ptr, int64_t n, int32_t wgt, int32_t *__restrict__ part,
-                            int64_t n_waves)
+// part[w] = first row r with row_ptr[r] + wgt * r >= w * cost, for
+// w < n_waves; part[n_waves] = n.  A wave then holds at most
+// cost / wgt + 1 <= rows_cap(dim) rows (cost rises by >= wgt per row) and
+// about cost edges unless its last row alone is longer.
+__global__ void k_partition(const int64_t *__restrict__ row_ptr, int64_t n, int32_t wgt, int64_t cost,
+                            int32_t *__restrict__ part, int64_t n_waves)
 {
     const int64_t w = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (w > n_waves) return;
@@ -323,7 +323,7 @@ __global__ void k_partition(const int64_t *__restrict__ row_ptr, int64_t n, int3
         part[w] = (int32_t)n;
         return;
     }
-    const int64_t target = w * (int64_t)kWaveCost;
+    const int64_t target = w * cost;
     int64_t lo = 0, hi = n;
     while (lo < hi) {
         int64_t mid = (lo + hi) >> 1;
@@ -348,12 +348,13 @@ __global__ void k_head_local(const int64_t *__restrict__ row_ptr, int64_t n, con
     for (int64_t e = row_ptr[r]; e < row_ptr[r + 1]; ++e) head[e] = h;
 }
 
-hipError_t launch_partition(const int64_t *row_ptr, int64_t n, int32_t dim, int32_t *part, int64_t n_waves,
-                            uint8_t *head, hipStream_t s)
+hipError_t launch_partition(const int64_t *row_ptr, int64_t n, int32_t dim, int64_t cost, int32_t *part,
+                            int64_t n_waves, uint8_t *head, hipStream_t s)
 {
+    if (cost < 1 || cost > kWaveCost) return hipErrorInvalidValue;
     static_assert(rows_cap(1) <= 256 && rows_cap(16) <= 256, "head offsets must fit in a byte");
     int64_t blocks = (n_waves + 1 + 255) / 256;
-    hipLaunchKernelGGL(k_partition, dim3((unsigned)blocks), dim3(256), 0, s, row_ptr, n, row_weight(dim), part,
+    hipLaunchKernelGGL(k_partition, dim3((unsigned)blocks), dim3(256), 0, s, row_ptr, n, row_weight(dim), cost, part,
                        n_waves);
     hipLaunchKernelGGL(k_head_local, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, row_ptr, n, part, n_waves,
                        head);
