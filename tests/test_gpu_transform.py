@@ -162,3 +162,30 @@ def test_transform_quality_blobs():
     assert acc_g >= 0.95
     assert abs(acc_g - acc_o) <= 0.01
     assert abs(tg - to) <= 0.01
+
+
+def test_transform_edge_cases():
+    """New points without kept edges start at the origin and never move; an
+    empty graph leaves every new point at the origin; weights of zero are
+    dropped."""
+    T = synth.embedding_state(100, 2, 21, 10.0)
+    a, b = O.fit_ab(1.0, 0.1)
+    rows = np.array([0, 0, 3, 3, 3, 4], np.int32)
+    cols = np.array([5, 7, 10, 11, 99, 50], np.int32)
+    vals = np.array([1.0, 0.5, 0.25, 1.0, 0.75, 0.0], np.float32)   # row 4's only entry has weight 0
+    g = O.prep_bipartite(5, 100, rows, cols, vals, 20)
+    case("transform edge cases")
+    with U.umap_transform_create(5, T, rows, cols, vals, a, b, 20, 5) as h:
+        _check_graph(h, g)
+        U.umap_layout_init(h, 3)
+        assert float(np.abs(U.umap_layout_get(h) - O.transform_init(g, T)).max()) <= 1e-5
+        U.umap_layout_run(h, 3)
+        Y = U.umap_layout_get(h)
+        assert np.all(np.isfinite(Y))
+        assert np.array_equal(Y[[1, 2, 4]], np.zeros((3, 2), np.float32))
+        assert U.umap_layout_stats(h)["nnz_kept"] == 5
+    empty = np.zeros(0, np.int32)
+    with U.umap_transform_create(3, T, empty, empty, np.zeros(0, np.float32), a, b, 10, 5) as h:
+        U.umap_layout_run(h, 1)
+        assert np.array_equal(U.umap_layout_get(h), np.zeros((3, 2), np.float32))
+        assert U.umap_layout_stats(h)["active_edges"] == 0
