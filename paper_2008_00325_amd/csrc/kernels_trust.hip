@@ -99,27 +99,35 @@ __global__ __launch_bounds__(256) void k_tw_embed_knn(const float *__restrict__ 
     if (lane < k) nbr[i * k + lane] = bi;
 }
 
-// A neighbour slot left unfilled (a non-finite embedding coordinate never
-// compares below the running threshold) raises `flags` and gets a threshold
-// that nothing counts against.
+// One wavefront per point i: the input distance to each of its k embedding
+// neighbours (lanes split the features, coalesced rows).  A neighbour slot
+// left unfilled (a non-finite embedding coordinate never compares below the
+// running threshold) raises `flags` and gets a threshold that nothing counts
+// against.
 __global__ __launch_bounds__(256) void k_tw_thresholds(const float *__restrict__ X, int64_t n, int32_t d, int32_t k,
                                                        const float *__restrict__ nx, const int32_t *__restrict__ nbr,
                                                        float *__restrict__ thr, unsigned *__restrict__ flags)
 {
-    const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (t >= n * k) return;
-    const int64_t i = t / k;
-    const int64_t j = nbr[t];
-    if (j < 0 || j >= n) {
-        thr[t] = -INFINITY;
-        atomicOr(flags, 1u);
-        return;
-    }
+    const int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) / kWave;
+    const int lane = threadIdx.x % kWave;
+    if (i >= n) return;   // whole waves
     const float *xi = X + i * d;
-    const float *xj = X + j * d;
-    float dot = 0.0f;
-    for (int32_t q = 0; q < d; ++q) dot = fmaf(xi[q], xj[q], dot);
-    thr[t] = nx[i] + nx[j] - 2.0f * dot;
+    for (int32_t s = 0; s < k; ++s) {
+        const int64_t j = nbr[i * k + s];   // the same for every lane
+        if (j < 0 || j >= n) {
+            if (lane == 0) {
+                thr[i * k + s] = -INFINITY;
+                atomicOr(flags, 1u);
+            }
+            continue;
+        }
+        const float *xj = X + j * d;
+        float dot = 0.0f;
+        for (int32_t q = lane; q < d; q += kWave) dot = fmaf(xi[q], xj[q], dot);
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) dot += __shfl_xor(dot, off);
+        if (lane == 0) thr[i * k + s] = nx[i] + nx[j] - 2.0f * dot;
+    }
 }
 
 // Input distances of a block of kRkRows points (rows) to a range of column
@@ -364,8 +372,8 @@ hipError_t launch_trustworthiness(const float *X, int64_t n, int32_t d, const fl
     default: return hipErrorInvalidValue;
     }
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_tw_thresholds, dim3((unsigned)((n * k + 255) / 256)), dim3(256), 0, s, X, n, d, k, nx, nbr,
-                       thr, flags);
+    hipLaunchKernelGGL(k_tw_thresholds, dim3((unsigned)((n * kWave + 255) / 256)), dim3(256), 0, s, X, n, d, k, nx,
+                       nbr, thr, flags);
     const int64_t nk = n * k;
     hipLaunchKernelGGL(k_tw_zero, dim3((unsigned)((nk + 255) / 256 < 4096 ? (nk + 255) / 256 : 4096)), dim3(256), 0,
                        s, cnt, nk);
