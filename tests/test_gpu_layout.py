@@ -333,7 +333,7 @@ def test_full_run_quality_window(name, mode):
         assert obj <= 1.01 * ref["objective"]
 
 
-@pytest.mark.parametrize("dim,R,N", [(1, 5, 20), (3, 5, 200), (4, 0, 50), (16, 7, 30)])
+@pytest.mark.parametrize("dim,R,N", [(1, 5, 20), (3, 5, 200), (4, 0, 50), (16, 7, 30), (2, 12, 40)])
 def test_single_epoch_dims_and_rates(dim, R, N):
     n = 5003
     bounds = synth.cluster_bounds(n, 3)
