@@ -21,7 +21,7 @@ namespace {
 
 thread_local std::string g_err;
 
-int fail(int code, const char *fmt, ...)
+__attribute__((format(printf, 2, 3))) int fail(int code, const char *fmt, ...)
 {
     char buf[512];
     va_list ap;
@@ -153,10 +153,10 @@ struct umap_layout {
 
     void release()
     {
-        if (stream || arena) hipStreamSynchronize(stream);
+        if (stream || arena) (void)hipStreamSynchronize(stream);
         for (auto &e : ev)
-            if (e) hipEventDestroy(e);
-        if (arena) hipFree(arena);
+            if (e) (void)hipEventDestroy(e);
+        if (arena) (void)hipFree(arena);
         arena = nullptr;
     }
 };
@@ -318,12 +318,12 @@ int create_common(umap_layout **out, int64_t n, int32_t dim, const int32_t *rows
         return UMAP_OK;
     } catch (const HipFailure &f) {
         int rc = hip_fail(f);
-        if (scratch) hipFreeAsync(scratch, stream);
+        if (scratch) (void)hipFreeAsync(scratch, stream);
         h->release();
         delete h;
         return rc;
     } catch (...) {
-        if (scratch) hipFreeAsync(scratch, stream);
+        if (scratch) (void)hipFreeAsync(scratch, stream);
         h->release();
         delete h;
         return fail(UMAP_E_NOMEM, "unexpected host failure");
@@ -689,7 +689,7 @@ int umap_layout_set_mode(umap_layout *h, int32_t mode)
 void umap_layout_destroy(umap_layout *h)
 {
     if (!h) return;
-    hipSetDevice(h->device);
+    (void)hipSetDevice(h->device);
     h->release();
     delete h;
 }
@@ -710,7 +710,7 @@ int umap_layout_debug_active(const umap_layout *h, int32_t epoch, uint8_t *out)
         UL_HIP(hipStreamSynchronize(h->stream));
         return UMAP_OK;
     } catch (const HipFailure &f) {
-        if (d) hipFreeAsync(d, h->stream);
+        if (d) (void)hipFreeAsync(d, h->stream);
         return hip_fail(f);
     }
 }
@@ -735,7 +735,7 @@ int umap_layout_debug_negatives(const umap_layout *h, uint64_t seed, int32_t epo
         UL_HIP(hipStreamSynchronize(h->stream));
         return UMAP_OK;
     } catch (const HipFailure &f) {
-        if (d) hipFreeAsync(d, h->stream);
+        if (d) (void)hipFreeAsync(d, h->stream);
         return hip_fail(f);
     }
 }
@@ -771,7 +771,7 @@ int umap_fuzzy_graph_device(int64_t n, int32_t k, const int32_t *knn_ids, const 
         if (hflags & ul::kBadValue) return fail(UMAP_E_INVAL, "a neighbour distance is not finite");
         return UMAP_OK;
     } catch (const HipFailure &f) {
-        if (scratch) hipFreeAsync(scratch, s);
+        if (scratch) (void)hipFreeAsync(scratch, s);
         return hip_fail(f);
     }
 }
@@ -817,14 +817,14 @@ int umap_trustworthiness(const float *X, int64_t n, int32_t d, const float *Y, i
         *out = 1.0 - 2.0 / (nn * kk * (2.0 * nn - 3.0 * kk - 1.0)) * (double)hsum;
         return UMAP_OK;
     } catch (const HipFailure &f) {
-        if (scratch) hipFreeAsync(scratch, s);
+        if (scratch) (void)hipFreeAsync(scratch, s);
         return hip_fail(f);
     }
 }
 
 int umap_probe_copy(const void *src, void *dst, int64_t bytes, void *stream)
 {
-    if (!src || !dst || bytes < 0 || bytes % 16) return fail(UMAP_E_INVAL, "need non-NULL pointers and bytes % 16 == 0");
+    if (!src || !dst || bytes < 0 || bytes % 16) return fail(UMAP_E_INVAL, "need non-NULL pointers and bytes %% 16 == 0");
     try {
         UL_HIP(ul::launch_probe_copy(src, dst, bytes, static_cast<hipStream_t>(stream)));
         return UMAP_OK;
