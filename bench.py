@@ -159,6 +159,50 @@ def async_mode(w, torch, U, coo, a, b, reps: int = 3) -> dict:
     }
 
 
+def shard_measure(w, U, coo, a, b, parts: int = 8, reps: int = 3) -> dict:
+    """One GPU's share of a layout sharded by contiguous row ranges of about
+    equal kept edges (each GPU would read the whole snapshot and write its
+    rows; an all-gather of the rows would end each epoch): the epochs of each
+    range on this GPU, outside the timed steps, median device time over `reps`
+    runs.  The slowest range bounds the epoch of a sharded run."""
+    rows, cols, vals = coo
+    with U.umap_layout_create_device(w.n, w.dim, rows, cols, vals, rows.numel(), a, b, w.n_epochs, w.neg_rate) as h:
+        row_ptr, _, _ = U.umap_layout_get_graph(h)
+        nnz = int(row_ptr[-1])
+        bounds = np.searchsorted(row_ptr, (np.arange(parts + 1, dtype=np.int64) * nnz) // parts, side="left")
+        bounds[0], bounds[-1] = 0, w.n
+        full = []
+        for s in range(reps):
+            U.umap_layout_run(h, 4000 + s)
+            full.append(U.umap_layout_stats(h)["epochs_ms"])
+        shards = []
+        for p in range(parts):
+            r0, r1 = int(bounds[p]), int(bounds[p + 1])
+            U.umap_layout_set_rows(h, r0, r1)
+            runs = []
+            for s in range(reps):
+                U.umap_layout_run(h, 4000 + s)
+                runs.append(U.umap_layout_stats(h))
+            ms = float(np.median([x["epochs_ms"] for x in runs]))
+            shards.append({"rows": [r0, r1], "edges": int(row_ptr[r1] - row_ptr[r0]), "epochs_ms": ms,
+                           "waves": runs[-1]["n_waves"],
+                           "edge_updates_per_s": runs[-1]["edge_updates"] / (ms * 1e-3)})
+        U.umap_layout_set_rows(h, 0, w.n)
+    full_ms = float(np.median(full))
+    slowest = max(x["epochs_ms"] for x in shards)
+    log(f"row ranges: {parts} shares, slowest {slowest:.2f} ms vs {full_ms:.2f} ms for all rows")
+    return {
+        "parts": parts,
+        "all_rows_epochs_ms": full_ms,
+        "slowest_share_epochs_ms": slowest,
+        "share_efficiency": full_ms / (parts * slowest),
+        "shares": shards,
+        "note": "each share's epochs run alone on this GPU, gathering from the full snapshot (rows outside the "
+                "range held fixed); no all-gather and no second GPU are involved; share_efficiency = all-rows "
+                "time / (parts x slowest share)",
+    }
+
+
 def transform_measure(w, U, table: np.ndarray, a: float, b: float, n_new: int = 100_000, n_epochs: int = 100,
                       reps: int = 3) -> dict:
     """A transform of n_new new points against the fit's layout (frozen),
@@ -347,9 +391,10 @@ def main() -> int:
     launch_ms = epochs_ms / n_epochs
     achieved = bytes_epoch / (launch_ms * 1e-3) / 1e9
     traffic = profiled_traffic(w.name)
-    async_stats = transform_stats = trust_stats = None
+    async_stats = transform_stats = trust_stats = shard_stats = None
     if not args.no_extras:
         async_stats = async_mode(w, torch, U, (rows, cols, vals), a, b)
+        shard_stats = shard_measure(w, U, (rows, cols, vals), a, b)
         transform_stats = transform_measure(w, U, gpu_steps.layout.cpu().numpy(), a, b)
         trust_stats = trustworthiness_measure(torch, U)
     copy_gbps = copy_probe(torch, U)
@@ -407,8 +452,8 @@ def main() -> int:
                     f"vertex-table range, the slice one repulsion launch gathers from); the probe on the whole "
                     f"{w.n * w.dim * 4 / 1e6:.0f} MB table reaches {gather_full / 1e9:.0f} G/s",
         },
-        **({} if args.no_extras else {"async_mode": async_stats, "transform": transform_stats,
-                                       "trustworthiness": trust_stats}),
+        **({} if args.no_extras else {"async_mode": async_stats, "row_shares": shard_stats,
+                                       "transform": transform_stats, "trustworthiness": trust_stats}),
         "fuzzy_graph_ms": build_input.fuzzy_graph_ms,
         "hbm_copy_probe_GBps": copy_gbps,
         "gpu": gpu_name,

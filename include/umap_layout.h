@@ -77,6 +77,9 @@ typedef struct {
                                sample found its record slot full (the result is
                                the same bit for bit; only the time is lost)    */
     int32_t mode;           /* UMAP_MODE_SYNC or UMAP_MODE_ASYNC                 */
+    int64_t row_first;      /* rows the epochs update: [row_first, row_last)     */
+    int64_t row_last;       /*   (umap_layout_set_rows; 0 and n by default)      */
+    int64_t n_waves;        /* waves of an edge-parallel epoch launch            */
 } umap_layout_stats_t;
 
 /*
@@ -257,6 +260,23 @@ int umap_layout_set_kernel(umap_layout *h, int32_t which);
  *                    (UMAP_E_INVAL from the run otherwise).
  * Any other value is UMAP_E_INVAL.  Takes effect at the next run. */
 int umap_layout_set_mode(umap_layout *h, int32_t mode);
+
+/* umap_layout_set_rows -- later epochs update only the rows [row_first,
+ * row_last): one GPU's share of a layout sharded by contiguous row ranges.
+ * The epoch of the embedding-updates section (epoch-synchronous reading) is a
+ * sum of terms per row, each read from the snapshot E_n; a GPU that owns a
+ * range computes its rows' sums from a full replica of E_n, and an
+ * all-gather of the rows would end the epoch.  Here the rows outside the
+ * range keep their values (they stand for the rows other GPUs own).  The
+ * negative samples are still drawn from all vertices and keyed by the global
+ * edge ids, and the sums are exact, so each row of the range is bit-identical
+ * to the same row of an epoch over all rows from the same layout.  The waves
+ * of the edge-parallel kernel are re-cut for the range (the same cost rule
+ * applied to its edges and rows); init still sets every row.  Synchronous
+ * mode only (a run in UMAP_MODE_ASYNC with a range is UMAP_E_INVAL).
+ * umap_layout_set_rows(h, 0, n) restores the default.  Errors: UMAP_E_INVAL
+ * unless 0 <= row_first < row_last <= n; UMAP_E_DEVICE.  Blocking. */
+int umap_layout_set_rows(umap_layout *h, int64_t row_first, int64_t row_last);
 
 /* ---- quality ------------------------------------------------------------- */
 

@@ -135,6 +135,8 @@ struct umap_layout {
     float *eps = nullptr;
     int32_t *part = nullptr;
     int64_t n_waves = 0;
+    int64_t max_waves = 0;                  // capacity of part, rec_count and the record slots
+    int64_t row_first = 0, row_last = 0;    // rows the epochs update (umap_layout_set_rows)
     uint8_t *head = nullptr;       // edge's row relative to its wave's first row
     float *E[2] = {nullptr, nullptr};
     int cur = 0;
@@ -189,11 +191,14 @@ int create_common(umap_layout **out, int64_t n, int32_t dim, const int32_t *rows
         h->neg_rate = neg_rate;
         h->nnz_in = nnz;
         h->n_table = table ? n_table : n;
+        h->row_first = 0;
+        h->row_last = n;
         for (auto &e : h->ev) UL_HIP(hipEventCreate(&e));
 
         // persistent arena; the wave count is bounded with nnz (kept <= nnz)
         const int wgt = ul::row_weight(dim);
         const int64_t max_waves = ul::max_wave_count(nnz + (int64_t)wgt * n);
+        h->max_waves = max_waves;
         const size_t nd = (size_t)n * (size_t)dim;
         const int64_t count_stride =
             ul::count_slots(1, n, 0) > max_waves ? ul::count_slots(1, n, 0) : max_waves;
@@ -310,7 +315,7 @@ int create_common(umap_layout **out, int64_t n, int32_t dim, const int32_t *rows
         h->n_waves = (units + cost - 1) / cost;
         if (h->n_waves < 1) h->n_waves = 1;
         if (h->n_waves > max_waves) throw HipFailure{hipErrorInvalidValue, "wave count exceeds the arena"};
-        UL_HIP(ul::launch_partition(h->row_ptr, n, dim, cost, h->part, h->n_waves, h->head, stream));
+        UL_HIP(ul::launch_partition(h->row_ptr, 0, n, dim, cost, h->part, h->n_waves, h->head, stream));
         float ms = 0;
         UL_HIP(hipEventElapsedTime(&ms, h->ev[0], h->ev[1]));
         h->st.prep_ms = ms;
@@ -335,6 +340,8 @@ int run_epochs_impl(umap_layout *h, uint64_t seed, int32_t first, int32_t last, 
     const int fault = fault_launch_epoch();
     ul::EpochArgs A{};
     A.n = (uint32_t)h->n;
+    A.row_first = (uint32_t)h->row_first;
+    A.row_last = (uint32_t)h->row_last;
     A.n_table = (uint32_t)h->n_table;
     A.same_table = h->table ? 0 : 1;
     A.attr_mult = h->table ? 1.0f : 2.0f;
@@ -355,6 +362,8 @@ int run_epochs_impl(umap_layout *h, uint64_t seed, int32_t first, int32_t last, 
                       (int64_t)h->max_degree + ul::kWaveCost < ((int64_t)1 << 24);
     const bool async = h->mode == 1;
     if (async && h->table) return fail(UMAP_E_INVAL, "the asynchronous mode applies to fits, not to transforms");
+    const bool restricted = h->row_first > 0 || h->row_last < h->n;
+    if (async && restricted) return fail(UMAP_E_INVAL, "the asynchronous mode updates all rows (umap_layout_set_rows)");
     if (async && (int64_t)h->max_degree + ul::kWaveCost >= ((int64_t)1 << 24))
         return fail(UMAP_E_INVAL, "the asynchronous mode needs rows of fewer than %d edges",
                     (1 << 24) - ul::kWaveCost);
@@ -364,7 +373,18 @@ int run_epochs_impl(umap_layout *h, uint64_t seed, int32_t first, int32_t last, 
     const int kernel = async ? kAsyncKernel : fits ? h->kernel : 1;
     const bool records = kernel == 0;
     const int cur0 = h->cur;
-    const size_t nd_bytes = sizeof(float) * (size_t)h->n * (size_t)h->dim;
+    const size_t row_bytes = sizeof(float) * (size_t)h->dim;
+    const size_t nd_bytes = row_bytes * (size_t)h->n;
+    if (restricted && !async) {
+        // rows outside the range are not written by the epochs: make both
+        // buffers hold them, so that they keep their values
+        float *src = h->E[cur0], *dst = h->E[1 - cur0];
+        if (h->row_first > 0)
+            UL_HIP(hipMemcpyAsync(dst, src, row_bytes * (size_t)h->row_first, hipMemcpyDeviceToDevice, h->stream));
+        if (h->row_last < h->n)
+            UL_HIP(hipMemcpyAsync(dst + (size_t)h->row_last * h->dim, src + (size_t)h->row_last * h->dim,
+                                  row_bytes * (size_t)(h->n - h->row_last), hipMemcpyDeviceToDevice, h->stream));
+    }
     if (records) {
         // the layout this call starts from, in case a record slot overflows
         UL_HIP(hipMemsetAsync(h->overflow, 0, sizeof(unsigned), h->stream));
@@ -375,7 +395,7 @@ int run_epochs_impl(umap_layout *h, uint64_t seed, int32_t first, int32_t last, 
     // epochs [first, last) with one kernel; fault >= 0 injects a launch error
     auto epochs = [&](int which) -> int {
         UL_HIP(ul::launch_zero_u64(h->active, h->n_epochs, h->stream));
-        const int64_t slots = ul::count_slots(which == 1 ? 1 : 0, h->n, h->n_waves);
+        const int64_t slots = ul::count_slots(which == 1 ? 1 : 0, h->row_last - h->row_first, h->n_waves);
         const int ring = h->n_epochs < ul::kCountRing ? h->n_epochs : ul::kCountRing;
         int32_t pending_from = first;   // first epoch whose counts are not yet summed
         for (int32_t ep = first; ep < last; ++ep) {
@@ -653,6 +673,9 @@ int umap_layout_stats(const umap_layout *h, umap_layout_stats_t *out)
     s.table_ranges = 1 << h->lg_phases;
     s.kernel = h->kernel;
     s.mode = h->mode;
+    s.row_first = h->row_first;
+    s.row_last = h->row_last;
+    s.n_waves = h->n_waves;
     *out = s;
     return UMAP_OK;
 }
@@ -675,6 +698,37 @@ int umap_layout_set_kernel(umap_layout *h, int32_t which)
     if (which != 0 && which != 1) return fail(UMAP_E_INVAL, "kernel must be 0 or 1, got %d", which);
     h->kernel = which;
     return UMAP_OK;
+}
+
+int umap_layout_set_rows(umap_layout *h, int64_t row_first, int64_t row_last)
+{
+    if (!h) return fail(UMAP_E_INVAL, "handle is NULL");
+    if (row_first < 0 || row_first >= row_last || row_last > h->n)
+        return fail(UMAP_E_INVAL, "need 0 <= row_first < row_last <= n (%lld), got %lld, %lld", (long long)h->n,
+                    (long long)row_first, (long long)row_last);
+    try {
+        UL_HIP(hipSetDevice(h->device));
+        // the waves of the range: the same cost rule as for the whole graph,
+        // applied to the range's units
+        int64_t ends[2] = {0, 0};
+        UL_HIP(hipMemcpyAsync(&ends[0], h->row_ptr + row_first, sizeof(int64_t), hipMemcpyDeviceToHost, h->stream));
+        UL_HIP(hipMemcpyAsync(&ends[1], h->row_ptr + row_last, sizeof(int64_t), hipMemcpyDeviceToHost, h->stream));
+        UL_HIP(hipStreamSynchronize(h->stream));
+        const int64_t units = ends[1] - ends[0] + (int64_t)ul::row_weight(h->dim) * (row_last - row_first);
+        const int64_t cost = ul::wave_cost(units);
+        int64_t waves = (units + cost - 1) / cost;
+        if (waves < 1) waves = 1;
+        if (waves > h->max_waves) return fail(UMAP_E_INVAL, "the range needs more waves than the handle holds");
+        UL_HIP(ul::launch_partition(h->row_ptr, row_first, row_last, h->dim, cost, h->part, waves, h->head,
+                                    h->stream));
+        UL_HIP(hipStreamSynchronize(h->stream));
+        h->n_waves = waves;
+        h->row_first = row_first;
+        h->row_last = row_last;
+        return UMAP_OK;
+    } catch (const HipFailure &f) {
+        return hip_fail(f);
+    }
 }
 
 int umap_layout_set_mode(umap_layout *h, int32_t mode)

@@ -82,8 +82,10 @@ struct PrepBuffers {
 
 int64_t scan_blocks(int64_t n);
 hipError_t launch_prep(const PrepBuffers &B, hipStream_t s);
-hipError_t launch_partition(const int64_t *row_ptr, int64_t n, int32_t dim, int64_t cost, int32_t *part,
-                            int64_t n_waves, uint8_t *head, hipStream_t s);
+// Waves over rows [r0, r1) (0 <= r0 < r1); n_waves = ceil(units / cost) for
+// the units (edges + row_weight x rows) of the range.
+hipError_t launch_partition(const int64_t *row_ptr, int64_t r0, int64_t r1, int32_t dim, int64_t cost,
+                            int32_t *part, int64_t n_waves, uint8_t *head, hipStream_t s);
 hipError_t launch_zero_u64(unsigned long long *p, int64_t count, hipStream_t s);
 
 // ---- layout (kernels_layout.hip) ----

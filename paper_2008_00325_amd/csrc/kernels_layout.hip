@@ -91,9 +91,9 @@ __global__ __launch_bounds__(256) void k_epoch_rowwise(EpochArgs A, const int64_
                                                        const int32_t *__restrict__ col,
                                                        const float *__restrict__ eps)
 {
-    const uint32_t i = blockIdx.x * 256u + threadIdx.x;
+    const uint32_t i = A.row_first + blockIdx.x * 256u + threadIdx.x;
     unsigned long long cnt = 0;
-    if (i < A.n) {
+    if (i < A.row_last) {
         float yi[DIM];
         load_row<DIM>(A.E, i, yi);
         long long acc[DIM];
@@ -414,7 +414,7 @@ template <int DIM, int NQ>
 static hipError_t launch_epoch_dq(int kernel, const EpochArgs &A, const WaveGraph &G, hipStream_t s)
 {
     if (kernel == 1) {
-        int64_t blocks = ((int64_t)A.n + 255) / 256;
+        const int64_t blocks = ((int64_t)A.row_last - A.row_first + 255) / 256;
         hipLaunchKernelGGL((k_epoch_rowwise<DIM, NQ>), dim3((unsigned)blocks), dim3(256), 0, s, A, G.row_ptr, G.col,
                            G.eps);
         return hipGetLastError();

@@ -314,17 +314,19 @@ hipError_t launch_prep(const PrepBuffers &B, hipStream_t s)
 // w < n_waves; part[n_waves] = n.  A wave then holds at most
 // cost / wgt + 1 <= rows_cap(dim) rows (cost rises by >= wgt per row) and
 // about cost edges unless its last row alone is longer.
-__global__ void k_partition(const int64_t *__restrict__ row_ptr, int64_t n, int32_t wgt, int64_t cost,
+// Waves over rows [r0, r1): part[w] is the first row r >= r0 whose units
+// (edges and row weights from r0 up to r) reach w x cost; part[n_waves] = r1.
+__global__ void k_partition(const int64_t *__restrict__ row_ptr, int64_t r0, int64_t r1, int32_t wgt, int64_t cost,
                             int32_t *__restrict__ part, int64_t n_waves)
 {
     const int64_t w = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (w > n_waves) return;
     if (w == n_waves) {
-        part[w] = (int32_t)n;
+        part[w] = (int32_t)r1;
         return;
     }
-    const int64_t target = w * cost;
-    int64_t lo = 0, hi = n;
+    const int64_t target = row_ptr[r0] + (int64_t)wgt * r0 + w * cost;
+    int64_t lo = r0, hi = r1;
     while (lo < hi) {
         int64_t mid = (lo + hi) >> 1;
         if (row_ptr[mid] + (int64_t)wgt * mid >= target) hi = mid; else lo = mid + 1;
@@ -333,12 +335,12 @@ __global__ void k_partition(const int64_t *__restrict__ row_ptr, int64_t n, int3
 }
 
 // head[e] = row of edge e minus the first row of its wave (< rows_cap <= 256).
-// One thread per row: its wave is the last w with part[w] <= row.
-__global__ void k_head_local(const int64_t *__restrict__ row_ptr, int64_t n, const int32_t *__restrict__ part,
-                             int64_t n_waves, uint8_t *__restrict__ head)
+// One thread per row of [r0, r1): its wave is the last w with part[w] <= row.
+__global__ void k_head_local(const int64_t *__restrict__ row_ptr, int64_t r0, int64_t r1,
+                             const int32_t *__restrict__ part, int64_t n_waves, uint8_t *__restrict__ head)
 {
-    const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (r >= n) return;
+    const int64_t r = r0 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (r >= r1) return;
     int64_t lo = 0, hi = n_waves - 1;
     while (lo < hi) {
         int64_t mid = (lo + hi + 1) >> 1;
@@ -348,16 +350,16 @@ __global__ void k_head_local(const int64_t *__restrict__ row_ptr, int64_t n, con
     for (int64_t e = row_ptr[r]; e < row_ptr[r + 1]; ++e) head[e] = h;
 }
 
-hipError_t launch_partition(const int64_t *row_ptr, int64_t n, int32_t dim, int64_t cost, int32_t *part,
-                            int64_t n_waves, uint8_t *head, hipStream_t s)
+hipError_t launch_partition(const int64_t *row_ptr, int64_t r0, int64_t r1, int32_t dim, int64_t cost,
+                            int32_t *part, int64_t n_waves, uint8_t *head, hipStream_t s)
 {
-    if (cost < 1 || cost > kWaveCost) return hipErrorInvalidValue;
+    if (cost < 1 || cost > kWaveCost || r0 < 0 || r1 <= r0 || n_waves < 1) return hipErrorInvalidValue;
     static_assert(rows_cap(1) <= 256 && rows_cap(16) <= 256, "head offsets must fit in a byte");
     int64_t blocks = (n_waves + 1 + 255) / 256;
-    hipLaunchKernelGGL(k_partition, dim3((unsigned)blocks), dim3(256), 0, s, row_ptr, n, row_weight(dim), cost, part,
-                       n_waves);
-    hipLaunchKernelGGL(k_head_local, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, row_ptr, n, part, n_waves,
-                       head);
+    hipLaunchKernelGGL(k_partition, dim3((unsigned)blocks), dim3(256), 0, s, row_ptr, r0, r1, row_weight(dim), cost,
+                       part, n_waves);
+    hipLaunchKernelGGL(k_head_local, dim3((unsigned)((r1 - r0 + 255) / 256)), dim3(256), 0, s, row_ptr, r0, r1, part,
+                       n_waves, head);
     return hipGetLastError();
 }
 

@@ -105,6 +105,8 @@ struct EpochArgs {
     float *E_next;       // E_{n+1}
     const float *T;      // table of tails and negative samples: E itself, or a frozen layout (transform)
     uint32_t n;
+    uint32_t row_first;  // rows [row_first, row_last) are updated (one GPU's share of a row-sharded
+    uint32_t row_last;   // layout); the wave kernels get them through their partition
     uint32_t n_table;    // rows of T; negative samples are drawn from [0, n_table)
     int32_t same_table;  // T is E: a draw equal to the source is skipped, near tails may come from LDS
     float attr_mult;     // 2 when the reverse edge's equal share lands on the row too (symmetric B), else 1

@@ -33,6 +33,7 @@ EXPORTS = (
     "umap_layout_get", "umap_layout_get_device", "umap_layout_set_embedding", "umap_layout_get_graph",
     "umap_layout_stats", "umap_layout_set_stream", "umap_layout_destroy", "umap_layout_last_error",
     "umap_layout_debug_active", "umap_layout_debug_negatives", "umap_layout_set_kernel", "umap_layout_set_mode",
+    "umap_layout_set_rows",
     "umap_fuzzy_graph_device", "umap_fit_ab", "umap_probe_copy", "umap_probe_gather",
     "umap_trustworthiness",
 )
@@ -58,6 +59,9 @@ class umap_layout_stats_t(ctypes.Structure):
         ("kernel", ctypes.c_int32),
         ("overflow_redone", ctypes.c_int32),
         ("mode", ctypes.c_int32),
+        ("row_first", ctypes.c_int64),
+        ("row_last", ctypes.c_int64),
+        ("n_waves", ctypes.c_int64),
     ]
 
     def as_dict(self) -> dict:
@@ -101,6 +105,7 @@ def lib() -> ctypes.CDLL:
             "umap_layout_debug_negatives": [P, u64, i32, i64, i64, P],
             "umap_layout_set_kernel": [P, i32],
             "umap_layout_set_mode": [P, i32],
+            "umap_layout_set_rows": [P, i64, i64],
             "umap_fuzzy_graph_device": [i64, i32, P, P, P, P, P, P],
             "umap_fit_ab": [f32, f32, ctypes.POINTER(f32), ctypes.POINTER(f32)],
             "umap_probe_copy": [P, P, i64, P],
@@ -271,6 +276,10 @@ def umap_layout_set_kernel(h: Handle, which: int) -> None:
 
 def umap_layout_set_mode(h: Handle, mode: int) -> None:
     _check(lib().umap_layout_set_mode(h.ptr, mode))
+
+
+def umap_layout_set_rows(h: Handle, row_first: int, row_last: int) -> None:
+    _check(lib().umap_layout_set_rows(h.ptr, row_first, row_last))
 
 
 def umap_layout_destroy(h: Handle) -> None:

@@ -99,6 +99,7 @@ int main(void)
     expect(umap_layout_set_stream(NULL, NULL), UMAP_E_INVAL, "NULL", "set_stream");
     expect(umap_layout_set_kernel(NULL, 0), UMAP_E_INVAL, "NULL", "set_kernel");
     expect(umap_layout_set_mode(NULL, 0), UMAP_E_INVAL, "NULL", "set_mode");
+    expect(umap_layout_set_rows(NULL, 0, 1), UMAP_E_INVAL, "NULL", "set_rows");
     expect(umap_layout_debug_active(NULL, 0, NULL), UMAP_E_INVAL, "NULL", "debug_active");
     expect(umap_layout_debug_negatives(NULL, 1, 0, 0, 1, NULL), UMAP_E_INVAL, "NULL", "debug_negatives");
     umap_layout_destroy(NULL);
