@@ -123,10 +123,17 @@ __host__ __device__ inline int64_t record_offset(int64_t w, int64_t e0, int32_t 
 
 // At most this many table ranges (phases) per epoch.
 constexpr int kMaxPhases = 16;
-// Table bytes per range: small enough to stay resident in one XCD's 4 MB L2
-// next to the streamed edge data.
+// The range count trades the gathers' L2 hit rate (a range of about 2 MB
+// stays resident in one XCD's 4 MB L2 next to the streamed edge data) against
+// the cost of each further range: one more launch and one more round trip of
+// the n x dim int64 partial sums.  Measured on 1M and 5M vertices with 2 to 16
+// components, the best count is 4 up to about 2.5M vertices and 8 at 5M,
+// whatever the row width, and never more than a 2 MB range needs.
 constexpr int64_t kPhaseTableBytes = 2 << 20;
-// log2 of the number of ranges for a table of n vertices x dim.
+constexpr int64_t kPhaseRows = 2500000;
+// log2 of the number of ranges for a table of n vertices x dim:
+// min(the ranges that bring a range to kPhaseTableBytes, 4 ranges per
+// kPhaseRows vertices rounded up to a power of two, kMaxPhases).
 int32_t phase_log2(int64_t n, int32_t dim);
 
 hipError_t launch_epoch(int kernel, int32_t dim, const EpochArgs &A, const WaveGraph &G, hipStream_t s);

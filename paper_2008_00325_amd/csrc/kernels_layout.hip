@@ -153,8 +153,11 @@ __global__ __launch_bounds__(256) void k_epoch_rowwise(EpochArgs A, const int64_
 // double buffered in registers: super-chunk s+1 is in flight while s is
 // classified.
 constexpr int kSuper = 2;
-// Records per lane per step of the repulsion kernel.
-constexpr int kRepUnroll = 16;
+// Records per lane per step of the repulsion kernel: all of a step's gathers
+// are in flight at once; fewer for wide rows, so that the two DIM-vectors per
+// record stay in registers at an occupancy of several waves per SIMD.
+template <int DIM>
+constexpr int rep_unroll() { return DIM <= 2 ? 16 : DIM <= 4 ? 8 : DIM <= 8 ? 4 : 2; }
 // LDS ring of sampled edges waiting for their attraction and draws: (tail,
 // (row in wave) << 24 | edge offset in wave); holds the < 64 left over plus
 // one super-chunk.
@@ -365,6 +368,7 @@ __global__ __launch_bounds__(256) void k_epoch_repulse(EpochArgs A, WaveGraph G,
     const uint32_t *recs = G.rec + roff + (int64_t)phase * cap;
     const uint32_t base = range_base((uint32_t)phase, G.lg_phases, A.n_table);
     // kRepUnroll records per lane per step, all loads issued before use
+    constexpr int kRepUnroll = rep_unroll<DIM>();
     for (int64_t b = 0; b < nrec; b += kRepUnroll * kWave) {
         uint32_t r[kRepUnroll];
 #pragma unroll
@@ -405,9 +409,11 @@ __global__ __launch_bounds__(256) void k_epoch_repulse(EpochArgs A, WaveGraph G,
 int32_t phase_log2(int64_t n, int32_t dim)
 {
     const int64_t bytes = n * dim * (int64_t)sizeof(float);
-    int32_t lg = 0;
-    while ((1 << (lg + 1)) <= kMaxPhases && (bytes >> lg) > kPhaseTableBytes) ++lg;
-    return lg;
+    int32_t lg_bytes = 0;   // the fewest ranges that bring a range down to kPhaseTableBytes
+    while ((1 << (lg_bytes + 1)) <= kMaxPhases && (bytes >> lg_bytes) > kPhaseTableBytes) ++lg_bytes;
+    int32_t lg_rows = 2;    // 4 ranges up to kPhaseRows vertices, twice as many per doubling of n beyond
+    while ((1 << (lg_rows + 1)) <= kMaxPhases && (n >> (lg_rows - 2)) > kPhaseRows) ++lg_rows;
+    return lg_bytes < lg_rows ? lg_bytes : lg_rows;
 }
 
 template <int DIM, int NQ>

@@ -248,8 +248,8 @@ def test_single_epoch_window1m_full_size(window1m_graph):
 
 @pytest.mark.parametrize("name", ["window1m_k30", "window5m"])
 def test_single_epoch_other_full_sizes(name):
-    """The two other full-size workloads: 1M vertices with k = 30 in 3-D (8
-    table ranges) and 5M vertices with lognormal cluster sizes (16 table
+    """The two other full-size workloads: 1M vertices with k = 30 in 3-D (4
+    table ranges) and 5M vertices with lognormal cluster sizes (8 table
     ranges); whole layout compared after one epoch fed the same fp32 state."""
     import torch
 
@@ -268,12 +268,40 @@ def test_single_epoch_other_full_sizes(name):
         _check_graph(h, g)
         st = U.umap_layout_stats(h)
         case(f"{name}: {st['table_ranges']} table ranges, {st['nnz_kept']} edges")
-        assert st["table_ranges"] == (8 if w.dim == 3 else 16)
+        assert st["table_ranges"] == (4 if w.n == 1_000_000 else 8)
         E = synth.embedding_state(w.n, w.dim, 6, 10.0)
         for kernel in (0, 1):
             U.umap_layout_set_kernel(h, kernel)
             _epoch_parity(h, g, E, (0, 1, w.n_epochs // 2, w.n_epochs - 1), a, b, w.n_epochs, w.neg_rate, 13,
                           f"{name} kernel {kernel} scale 10")
+
+
+def test_sixteen_table_ranges_sampled_rows():
+    """Past 5M vertices the table is split into 16 ranges: a sparse random
+    graph of 5.2M vertices, one epoch from a seeded state, 20,000 sampled
+    rows against the oracle's update of those rows (both kernels)."""
+    n, N, R, seed = 5_200_000, 50, 5, 17
+    case(f"{n} vertices: building a random graph")
+    r, c, v = synth.random_symmetric_coo(n, 4, 31)
+    g = O.prep(n, r, c, v, N)
+    E = synth.embedding_state(n, 2, 9, 10.0)
+    rows = np.sort(np.random.default_rng(5).choice(n, size=20_000, replace=False)).astype(np.int64)
+    with U.umap_layout_create(n, 2, r, c, v, A_DEF, B_DEF, N, R) as h:
+        assert U.umap_layout_stats(h)["table_ranges"] == 16
+        for kernel in (0, 1):
+            U.umap_layout_set_kernel(h, kernel)
+            for ep in (0, N // 2):
+                case(f"{n} vertices, 16 ranges, kernel {kernel} epoch {ep}")
+                U.umap_layout_set_embedding(h, E)
+                U.umap_layout_run_epochs(h, seed, ep, ep + 1)
+                got = U.umap_layout_get(h)
+                st = U.umap_layout_stats(h)
+                assert st["overflow_redone"] == 0
+                assert st["active_edges"] == int(O.active_mask(g.eps, ep).sum())
+                ref = E[rows].astype(np.float64) + O.epoch_rows(g, E, ep, A_DEF, B_DEF, N, R, seed, rows)
+                err = float(np.abs(got[rows].astype(np.float64) - ref).max())
+                print(f"  max|diff| = {err:.3e}", flush=True)
+                assert err <= TOL
 
 
 def _window_quality_golden():
@@ -333,7 +361,7 @@ def test_full_run_quality_window(name, mode):
         assert obj <= 1.01 * ref["objective"]
 
 
-@pytest.mark.parametrize("dim,R,N", [(1, 5, 20), (3, 5, 200), (4, 0, 50), (16, 7, 30), (2, 12, 40)])
+@pytest.mark.parametrize("dim,R,N", [(1, 5, 20), (3, 5, 200), (4, 0, 50), (6, 5, 25), (16, 7, 30), (2, 12, 40)])
 def test_single_epoch_dims_and_rates(dim, R, N):
     n = 5003
     bounds = synth.cluster_bounds(n, 3)
