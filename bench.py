@@ -20,6 +20,7 @@ Prints one JSON line on stdout.
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import hashlib
 import json
 import os
@@ -354,6 +355,8 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="window1m")
+    ap.add_argument("--n-components", type=int, default=0,
+                    help="embedding dimension in place of the workload's own (same graph)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the asynchronous-mode, transform and trustworthiness figures (profiling runs of "
@@ -375,6 +378,8 @@ def main() -> int:
         return 2
     torch.cuda.set_device(0)
     w = synth.WORKLOADS[args.workload]
+    if args.n_components:
+        w = dataclasses.replace(w, dim=args.n_components)
     ids, dist, rows, cols, vals, a, b = build_input(w, torch, U)
     stats, wall, finite = gpu_steps(w, torch, U, (rows, cols, vals), a, b, args.steps, args.warmup)
     if not finite:
