@@ -140,24 +140,28 @@ def gpu_steps(w, torch, U, coo, a, b, steps: int, warmup: int):
 
 def async_mode(w, torch, U, coo, a, b, reps: int = 3) -> dict:
     """The asynchronous (Hogwild) mode on the same input, outside the timed
-    steps: median device time of the epochs over `reps` runs."""
+    steps, with each of its two kernels: median device time of the epochs over
+    `reps` runs."""
     rows, cols, vals = coo
+    out = {}
     with U.umap_layout_create_device(w.n, w.dim, rows, cols, vals, rows.numel(), a, b, w.n_epochs, w.neg_rate) as h:
         U.umap_layout_set_mode(h, U.UMAP_MODE_ASYNC)
-        runs = []
-        for s in range(reps):
-            U.umap_layout_run(h, 2000 + s)
-            runs.append(U.umap_layout_stats(h))
-        finite = bool(np.isfinite(U.umap_layout_get(h)).all())
-    ms = float(np.median([r["epochs_ms"] for r in runs]))
-    log(f"asynchronous mode: epochs {ms:.2f} ms (median of {reps})")
-    return {
-        "epochs_ms": ms,
-        "edge_updates_per_s": runs[-1]["edge_updates"] / (ms * 1e-3),
-        "finite": finite,
-        "note": "asynchronous in-place (Hogwild) updates, one launch per epoch; not bit-repeatable, quality "
-                "checked by the tests (trustworthiness within 0.01 of the oracle's)",
-    }
+        for kernel, name in ((0, "range_ordered"), (1, "per_edge")):
+            U.umap_layout_set_kernel(h, kernel)
+            runs = []
+            for s in range(reps):
+                U.umap_layout_run(h, 2000 + s)
+                runs.append(U.umap_layout_stats(h))
+            finite = bool(np.isfinite(U.umap_layout_get(h)).all())
+            ms = float(np.median([r["epochs_ms"] for r in runs]))
+            log(f"asynchronous mode, {name} kernel: epochs {ms:.2f} ms (median of {reps})")
+            out[name] = {"epochs_ms": ms, "edge_updates_per_s": runs[-1]["edge_updates"] / (ms * 1e-3),
+                         "finite": finite}
+    out["note"] = ("asynchronous in-place (Hogwild) updates; range_ordered = the synchronous mode's launches "
+                   "adding their sums in place (the default), per_edge = one lane per sampled edge applying its "
+                   "attraction and negatives in turn; not bit-repeatable, quality checked by the tests "
+                   "(trustworthiness within 0.01 of the oracle's)")
+    return out
 
 
 def shard_measure(w, U, coo, a, b, parts: int = 8, reps: int = 3) -> dict:

@@ -238,7 +238,8 @@ int umap_layout_debug_negatives(const umap_layout *h, uint64_t seed, int32_t epo
 
 /* umap_layout_set_kernel -- choose the epoch kernel: 0 = edge-parallel
  * wavefront kernel (default), 1 = one thread per vertex.  Both compute the
- * same result bit for bit. */
+ * same result bit for bit.  In UMAP_MODE_ASYNC: 0 = range-ordered, 1 =
+ * per-edge (see umap_layout_set_mode). */
 int umap_layout_set_kernel(umap_layout *h, int32_t which);
 
 /* umap_layout_set_mode -- how later runs apply their updates (embedding-updates
@@ -246,18 +247,25 @@ int umap_layout_set_kernel(umap_layout *h, int32_t which);
  *   UMAP_MODE_SYNC   epoch-synchronous (default): E_{n+1} = E_n + alpha_n x
  *                    the sum of the epoch's terms, every term computed from
  *                    E_n; deterministic, bit-identical for both kernels.
- *   UMAP_MODE_ASYNC  asynchronous, in place (Hogwild): one thread per sampled
- *                    edge applies alpha_n x the clipped attraction to its
- *                    source (a private copy) and the opposite change to its
- *                    destination, then each negative sample's repulsion to
- *                    the private copy in turn, and adds the source's change
- *                    to the table; reads see whatever other threads have
- *                    written, so the result depends on the timing of the
- *                    GPU's threads and is not repeatable bit for bit.  Same
- *                    schedule, negative draws, clip and step size as the
- *                    synchronous mode; umap_layout_set_kernel does not apply.
- *                    Needs rows of fewer than 2^24 - 8192 edges
- *                    (UMAP_E_INVAL from the run otherwise).
+ *   UMAP_MODE_ASYNC  asynchronous, in place (Hogwild): updates land in the
+ *                    layout while the epoch runs and reads see whatever has
+ *                    been written, so the result depends on the timing of
+ *                    the GPU's threads and is not repeatable bit for bit.
+ *                    Same schedule, negative draws, clip and step size as
+ *                    the synchronous mode.  Two kernels (set_kernel):
+ *                    0 (default) range-ordered: the launches of a
+ *                      synchronous epoch (sampled edges with their
+ *                      attractions, then the negative samples of each table
+ *                      range) each add alpha_n x their sums to the rows they
+ *                      own as they finish;
+ *                    1 per-edge: one thread per sampled edge applies
+ *                      alpha_n x the clipped attraction to its source (a
+ *                      private copy) and the opposite change to its
+ *                      destination, then each negative sample's repulsion to
+ *                      the private copy in turn, and adds the source's
+ *                      change to the layout; needs rows of fewer than
+ *                      2^24 - 8192 edges (UMAP_E_INVAL from the run
+ *                      otherwise).
  * Any other value is UMAP_E_INVAL.  Takes effect at the next run. */
 int umap_layout_set_mode(umap_layout *h, int32_t mode);
 

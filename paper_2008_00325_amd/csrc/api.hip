@@ -364,13 +364,16 @@ int run_epochs_impl(umap_layout *h, uint64_t seed, int32_t first, int32_t last, 
     if (async && h->table) return fail(UMAP_E_INVAL, "the asynchronous mode applies to fits, not to transforms");
     const bool restricted = h->row_first > 0 || h->row_last < h->n;
     if (async && restricted) return fail(UMAP_E_INVAL, "the asynchronous mode updates all rows (umap_layout_set_rows)");
-    if (async && (int64_t)h->max_degree + ul::kWaveCost >= ((int64_t)1 << 24))
-        return fail(UMAP_E_INVAL, "the asynchronous mode needs rows of fewer than %d edges",
-                    (1 << 24) - ul::kWaveCost);
     // epoch kernel: 0 edge-parallel, 1 one thread per vertex, kAsyncKernel the
-    // asynchronous mode
+    // per-edge asynchronous kernel.  In the asynchronous mode kernel 0 runs in
+    // place (each launch adds its sums to the rows it owns) and kernel 1
+    // chooses the per-edge kernel, which is also taken where the 24-bit
+    // offsets of kernel 0 do not fit.
     constexpr int kAsyncKernel = -1;
-    const int kernel = async ? kAsyncKernel : fits ? h->kernel : 1;
+    const int kernel = async ? (fits && h->kernel == 0 ? 0 : kAsyncKernel) : fits ? h->kernel : 1;
+    if (kernel == kAsyncKernel && (int64_t)h->max_degree + ul::kWaveCost >= ((int64_t)1 << 24))
+        return fail(UMAP_E_INVAL, "the per-edge asynchronous kernel needs rows of fewer than %d edges",
+                    (1 << 24) - ul::kWaveCost);
     const bool records = kernel == 0;
     const int cur0 = h->cur;
     const size_t row_bytes = sizeof(float) * (size_t)h->dim;
@@ -412,10 +415,11 @@ int run_epochs_impl(umap_layout *h, uint64_t seed, int32_t first, int32_t last, 
                 UL_HIP(ul::launch_epoch_hogwild(h->dim, A, G, h->stream));
             } else {
                 A.E = h->E[h->cur];
-                A.E_next = h->E[1 - h->cur];
+                A.E_next = h->E[async ? h->cur : 1 - h->cur];
+                A.in_place = async ? 1 : 0;
                 A.T = h->table ? h->table : A.E;
                 UL_HIP(ul::launch_epoch(which, h->dim, A, G, h->stream));
-                h->cur = 1 - h->cur;
+                if (!async) h->cur = 1 - h->cur;
             }
             if (ep + 1 - pending_from == ring || ep + 1 == last) {
                 UL_HIP(ul::launch_reduce_counts(h->counts, h->count_stride, slots, ep + 1 - pending_from,
@@ -436,7 +440,8 @@ int run_epochs_impl(umap_layout *h, uint64_t seed, int32_t first, int32_t last, 
         if (overflow) {
             // a range slot was full: some negative samples were not applied;
             // redo the call's epochs from its starting layout with the
-            // one-thread-per-vertex kernel, which keeps no records
+            // one-thread-per-vertex kernel, which keeps no records (in place
+            // in the asynchronous mode)
             h->cur = cur0;
             UL_HIP(hipMemcpyAsync(h->E[cur0], h->E_start, nd_bytes, hipMemcpyDeviceToDevice, h->stream));
             rc = epochs(1);

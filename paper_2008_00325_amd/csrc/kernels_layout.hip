@@ -326,7 +326,11 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
     }
     wave_sync();
 
-    for (int t = lane; t < nrows * DIM; t += kWave) G.delta[g0 + t] = acc[t];
+    if (A.in_place) {
+        for (int t = lane; t < nrows * DIM; t += kWave) A.E_next[g0 + t] = commit(yrows[t], acc[t], A.alpha);
+    } else {
+        for (int t = lane; t < nrows * DIM; t += kWave) G.delta[g0 + t] = acc[t];
+    }
     if ((int)lane < G.n_phases) G.rec_count[(int64_t)lane * G.n_waves + w] = (int32_t)rec_n[lane];
     // per-wave count, summed by a separate pass (a global atomic per wave on
     // one address would serialise thousands of waves)
@@ -360,7 +364,7 @@ __global__ __launch_bounds__(256) void k_epoch_repulse(EpochArgs A, WaveGraph G,
     float *yrows = s_y[wv];
     const size_t g0 = (size_t)r0 * DIM;
     for (int t = lane; t < nrows * DIM; t += kWave) {
-        acc[t] = G.delta[g0 + t];
+        acc[t] = A.in_place ? 0ll : G.delta[g0 + t];
         yrows[t] = A.E[g0 + t];
     }
     wave_sync();
@@ -399,7 +403,7 @@ __global__ __launch_bounds__(256) void k_epoch_repulse(EpochArgs A, WaveGraph G,
     }
     wave_sync();
 
-    if (last) {
+    if (last || A.in_place) {
         for (int t = lane; t < nrows * DIM; t += kWave) A.E_next[g0 + t] = commit(yrows[t], acc[t], A.alpha);
     } else {
         for (int t = lane; t < nrows * DIM; t += kWave) G.delta[g0 + t] = acc[t];

@@ -109,6 +109,7 @@ struct EpochArgs {
     uint32_t row_last;   // layout); the wave kernels get them through their partition
     uint32_t n_table;    // rows of T; negative samples are drawn from [0, n_table)
     int32_t same_table;  // T is E: a draw equal to the source is skipped, near tails may come from LDS
+    int32_t in_place;    // asynchronous: E_next is E, and every launch adds its sums to the rows it owns
     float attr_mult;     // 2 when the reverse edge's equal share lands on the row too (symmetric B), else 1
     int32_t epoch;
     int32_t neg_rate;

@@ -313,8 +313,9 @@ def _window_quality_golden():
         return json.load(f)
 
 
-@pytest.mark.parametrize("name,mode", [("window1m", 0), ("window1m", 1), ("window1m_k30", 0), ("window5m", 0)])
-def test_full_run_quality_window(name, mode):
+@pytest.mark.parametrize("name,mode,kernel", [("window1m", 0, 0), ("window1m", 1, 0), ("window1m", 1, 1),
+                                               ("window1m_k30", 0, 0), ("window5m", 0, 0)])
+def test_full_run_quality_window(name, mode, kernel):
     """Full 200-epoch runs of the graph-only workloads, scored like the oracle's
     stored runs (same seed, same sample): recall@15 within 0.01 and the
     objective within 1 % of the oracle's.  The asynchronous mode (a different
@@ -336,10 +337,11 @@ def test_full_run_quality_window(name, mode):
     dr, dc, dv = (torch.from_numpy(x).cuda() for x in (r, c, v))
     nnz = r.size
     del r, c, v
-    case(f"{name} mode {mode}: GPU run")
+    case(f"{name} mode {mode} kernel {kernel}: GPU run")
     with U.umap_layout_create_device(w.n, w.dim, dr, dc, dv, nnz, a, b, w.n_epochs, w.neg_rate) as h:
         del dr, dc, dv
         U.umap_layout_set_mode(h, mode)
+        U.umap_layout_set_kernel(h, kernel)
         U.umap_layout_run(h, seed)
         E = U.umap_layout_get(h)
         st = U.umap_layout_stats(h)
@@ -443,25 +445,29 @@ def test_full_run_trustworthiness(blobs_graph):
         assert np.all(np.isfinite(Eg))
 
 
+@pytest.mark.parametrize("kernel", [0, 1])
 @pytest.mark.parametrize("dim,R", [(2, 5), (3, 5), (16, 10), (2, 0)])
-def test_async_mode_quality(dim, R, blobs_graph):
-    """Asynchronous (Hogwild) mode, the paper's default: not repeatable bit for
-    bit, so the check is on quality -- T@15 of a full run within 0.01 of the
-    oracle's (epoch-synchronous) run at the same settings -- plus the parts that
-    stay deterministic (the number of sampled edges, the mode switch)."""
+def test_async_mode_quality(dim, R, kernel, blobs_graph):
+    """Asynchronous (Hogwild) mode, the paper's default, with either kernel
+    (0 range-ordered, 1 per-edge): not repeatable bit for bit, so the check is
+    on quality -- T@15 of a full run within 0.01 of the oracle's
+    (epoch-synchronous) run at the same settings -- plus the parts that stay
+    deterministic (the number of sampled edges, the mode switch)."""
     w, X, ids, dist, (r, c, v) = blobs_graph
     g = O.prep(w.n, r, c, v, w.n_epochs)
     a, b = O.fit_ab(w.spread, w.min_dist)
     seed = 4
-    case(f"async blobs2k dim {dim} R {R}")
+    case(f"async blobs2k dim {dim} R {R} kernel {kernel}")
     with U.umap_layout_create(w.n, dim, r, c, v, a, b, w.n_epochs, R) as h:
         U.umap_layout_run(h, seed)
         Es = U.umap_layout_get(h)
         U.umap_layout_set_mode(h, U.UMAP_MODE_ASYNC)
+        U.umap_layout_set_kernel(h, kernel)
         U.umap_layout_run(h, seed)
         Ea = U.umap_layout_get(h)
         st = U.umap_layout_stats(h)
-        assert st["mode"] == U.UMAP_MODE_ASYNC
+        assert st["mode"] == U.UMAP_MODE_ASYNC and st["overflow_redone"] == 0
+        U.umap_layout_set_kernel(h, 0)
         with pytest.raises(U.UmapLayoutError) as ei:
             U.umap_layout_set_mode(h, 2)
         assert ei.value.code == U.UMAP_E_INVAL
