@@ -113,9 +113,12 @@ def test_graph_bit_exact_random(n, deg, N):
         _check_graph(h, g)
 
 
-def test_graph_hub_row():
-    # a star: vertex 0 joined to every other vertex (a row of n-1 edges)
-    n = 6000
+@pytest.mark.parametrize("n", [6000, 40001])
+def test_graph_hub_row(n):
+    """A star: vertex 0 joined to every other vertex (a row of n - 1 edges; at
+    40,001 vertices longer than a wave's whole cost, so the row is a wave of its
+    own), both kernels; the asynchronous mode's sampled-edge count and a finite
+    result."""
     others = np.arange(1, n, dtype=np.int32)
     vals = np.random.default_rng(3).random(n - 1).astype(np.float32) + np.float32(0.01)
     r = np.concatenate([np.zeros(n - 1, np.int32), others])
@@ -123,16 +126,29 @@ def test_graph_hub_row():
     v = np.concatenate([vals, vals])
     r, c, v = _shuffled((r, c, v), 2)
     g = O.prep(n, r, c, v, 100)
-    case("graph star n=6000")
+    case(f"graph star n={n}")
     with U.umap_layout_create(n, 2, r, c, v, A_DEF, B_DEF, 100, 5) as h:
         _check_graph(h, g)
+        assert U.umap_layout_stats(h)["max_degree"] == int(np.diff(g.row_ptr).max()) > 8192 * (n > 10000)
         E = synth.embedding_state(n, 2, 9)
-        for ep in (0, 50, 99):
+        for kernel in (0, 1):
+            U.umap_layout_set_kernel(h, kernel)
+            for ep in (0, 50, 99):
+                case(f"graph star n={n} kernel {kernel} epoch {ep}")
+                U.umap_layout_set_embedding(h, E)
+                U.umap_layout_run_epochs(h, 4, ep, ep + 1)
+                ref, act = O.epoch(g, E, ep, A_DEF, B_DEF, 100, 5, 4)
+                assert np.abs(U.umap_layout_get(h) - ref).max() <= TOL
+                st = U.umap_layout_stats(h)
+                assert st["active_edges"] == act and st["overflow_redone"] == 0
+        U.umap_layout_set_mode(h, U.UMAP_MODE_ASYNC)
+        for kernel in (0, 1):
+            U.umap_layout_set_kernel(h, kernel)
             U.umap_layout_set_embedding(h, E)
-            U.umap_layout_run_epochs(h, 4, ep, ep + 1)
-            ref, act = O.epoch(g, E, ep, A_DEF, B_DEF, 100, 5, 4)
-            assert np.abs(U.umap_layout_get(h) - ref).max() <= TOL
-            assert U.umap_layout_stats(h)["active_edges"] == act
+            U.umap_layout_run_epochs(h, 4, 0, 10)
+            assert np.all(np.isfinite(U.umap_layout_get(h)))
+            assert U.umap_layout_stats(h)["active_edges"] == sum(
+                int(O.active_mask(g.eps, ep).sum()) for ep in range(10))
 
 
 def test_graph_errors_on_device():
