@@ -36,12 +36,18 @@ __global__ __launch_bounds__(256) void k_dist_partial(const float *__restrict__ 
     if (threadIdx.x == 0) partial[blockIdx.x] = ((s_w[0] + s_w[1]) + s_w[2]) + s_w[3];
 }
 
-__global__ void k_dist_total(double *partial, int64_t np)
+// One block: thread t adds partials t, t + 256, ... in order, then a fixed
+// butterfly and a fixed sum over the four waves (the same order every call).
+__global__ __launch_bounds__(256) void k_dist_total(double *partial, int64_t np)
 {
-    if (threadIdx.x != 0 || blockIdx.x != 0) return;
     double s = 0.0;
-    for (int64_t b = 0; b < np; ++b) s += partial[b];
-    partial[np] = s;
+    for (int64_t b = threadIdx.x; b < np; b += 256) s += partial[b];
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
+    __shared__ double s_w[4];
+    if ((threadIdx.x & 63) == 0) s_w[threadIdx.x >> 6] = s;
+    __syncthreads();
+    if (threadIdx.x == 0) partial[np] = ((s_w[0] + s_w[1]) + s_w[2]) + s_w[3];
 }
 
 __device__ __forceinline__ double membership(double dist, double rho, double sigma)
@@ -128,7 +134,7 @@ hipError_t launch_fuzzy_graph(int64_t n, int32_t k, const int32_t *ids, const fl
 {
     const int64_t nk = n * k;
     hipLaunchKernelGGL(k_dist_partial, dim3((unsigned)npartial), dim3(256), 0, s, dists, nk, partial);
-    hipLaunchKernelGGL(k_dist_total, dim3(1), dim3(64), 0, s, partial, npartial);
+    hipLaunchKernelGGL(k_dist_total, dim3(1), dim3(256), 0, s, partial, npartial);
     hipLaunchKernelGGL(k_smooth, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, ids, dists, n, k, partial,
                        npartial, rho, sigma, flags);
     hipLaunchKernelGGL(k_union, dim3((unsigned)((nk + 255) / 256)), dim3(256), 0, s, ids, dists, n, k, rho, sigma,

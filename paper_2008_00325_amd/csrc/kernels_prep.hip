@@ -67,11 +67,21 @@ __global__ __launch_bounds__(256) void k_check_max(const int32_t *__restrict__ r
         if (!isfinite(v)) flags |= kBadValue;
         if (candidate(r, c, v, sh)) mx = max(mx, __float_as_uint(v));  // positive floats order as integers
     }
+    // one atomic per block: every block has a candidate weight, and atomics
+    // from thousands of waves on one address would serialise
     flags = wave_or(flags);
     mx = wave_max(mx);
+    __shared__ unsigned s_flags[4], s_max[4];
     if ((threadIdx.x & 63) == 0) {
-        if (flags) atomicOr(&S->flags, flags);
-        if (mx) atomicMax(&S->wmax_bits, mx);
+        s_flags[threadIdx.x >> 6] = flags;
+        s_max[threadIdx.x >> 6] = mx;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const unsigned f = s_flags[0] | s_flags[1] | s_flags[2] | s_flags[3];
+        const unsigned m = max(max(s_max[0], s_max[1]), max(s_max[2], s_max[3]));
+        if (f) atomicOr(&S->flags, f);
+        if (m) atomicMax(&S->wmax_bits, m);
     }
 }
 
@@ -235,11 +245,17 @@ __global__ __launch_bounds__(256) void k_row_sort(const int32_t *__restrict__ tr
         const int32_t r = trow[p];
         const int32_t c = tcol[p];
         const int64_t rs = row_ptr[r], re = row_ptr[r + 1];
+        // rank of c in its row; eight loads of the row in flight at a time
         int64_t rank = 0;
-        for (int64_t q = rs; q < re; ++q) {
-            int32_t cq = tcol[q];
-            rank += cq < c;
-            if (cq == c && q != p) flags |= kDuplicate;
+        for (int64_t q0 = rs; q0 < re; q0 += 8) {
+            int32_t cq[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) cq[u] = q0 + u < re ? tcol[q0 + u] : INT32_MAX;
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                rank += cq[u] < c;
+                if (cq[u] == c && q0 + u != p) flags |= kDuplicate;
+            }
         }
         const int64_t dst = rs + rank;
         const float v = tval[p];
@@ -293,7 +309,10 @@ hipError_t launch_prep(const PrepBuffers &B, hipStream_t s)
 {
     const IngestShape sh{(uint32_t)B.n, (uint32_t)B.n_cols, B.bipartite ? 1 : 0};
     const int64_t g = grid_for(B.nnz);
-    hipLaunchKernelGGL(k_check_max, dim3((unsigned)g), dim3(256), 0, s, B.rows, B.cols, B.vals, B.nnz, sh, B.scalars);
+    // a grid-stride pass with a block-wide reduction: 2048 blocks fill the chip
+    const int64_t g_check = g < 2048 ? g : 2048;
+    hipLaunchKernelGGL(k_check_max, dim3((unsigned)g_check), dim3(256), 0, s, B.rows, B.cols, B.vals, B.nnz, sh,
+                       B.scalars);
     hipLaunchKernelGGL(k_count, dim3((unsigned)g), dim3(256), 0, s, B.rows, B.cols, B.vals, B.nnz, sh, B.n_epochs,
                        B.scalars, B.deg);
     const int64_t nb = B.nblocks_scan;
