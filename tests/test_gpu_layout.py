@@ -419,6 +419,51 @@ def test_kernels_bit_identical_and_deterministic(window1m_graph):
         assert not np.array_equal(U.umap_layout_get(h), first)
 
 
+def test_two_handles_on_two_streams_in_parallel(window1m_graph):
+    """Two host threads, each driving its own handle on its own stream at the
+    same time (one with each kernel): every result equals the same run made
+    alone, bit for bit -- the library keeps no shared mutable state."""
+    import threading
+
+    import torch
+
+    w, ids, dist, (r, c, v) = window1m_graph
+    sub = (r < 200_000) & (c < 200_000)
+    r, c, v = r[sub], c[sub], v[sub]
+    n, N = 200_000, 30
+    seeds = (11, 12)
+    alone = {}
+    for s in seeds:
+        case(f"two streams: seed {s} alone")
+        with U.umap_layout_create(n, 2, r, c, v, A_DEF, B_DEF, N, 5) as h:
+            U.umap_layout_run(h, s)
+            alone[s] = U.umap_layout_get(h)
+    got, errors = {}, []
+
+    def worker(s, kernel):
+        try:
+            stream = torch.cuda.Stream()
+            with U.umap_layout_create(n, 2, r, c, v, A_DEF, B_DEF, N, 5) as h:
+                U.umap_layout_set_stream(h, stream)
+                U.umap_layout_set_kernel(h, kernel)
+                for _ in range(3):
+                    U.umap_layout_run(h, s)
+                got[s] = U.umap_layout_get(h)
+        except Exception as e:  # reported by the main thread
+            errors.append(e)
+
+    case("two streams: both seeds in parallel")
+    threads = [threading.Thread(target=worker, args=(s, k)) for s, k in zip(seeds, (0, 1))]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join(timeout=120)
+    assert not any(t.is_alive() for t in threads)
+    assert not errors, errors
+    for s in seeds:
+        assert np.array_equal(got[s].view(np.uint32), alone[s].view(np.uint32))
+
+
 def test_resume_equals_uninterrupted(blobs_graph):
     w, X, ids, dist, (r, c, v) = blobs_graph
     N = 60
