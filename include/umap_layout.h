@@ -126,7 +126,7 @@ int umap_layout_create_device(umap_layout **out, int64_t n, int32_t n_components
  * umap_layout_run -- random initial layout, uniform on [-10, 10) per
  * coordinate from the seed (embedding-updates section: random
  * initialisation), then epochs 0 .. N-1.  Same seed, same graph: bit-identical
- * output.  Blocking.
+ * output in the synchronous mode (UMAP_MODE_SYNC).  Blocking.
  */
 int umap_layout_run(umap_layout *h, uint64_t seed);
 
