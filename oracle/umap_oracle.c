@@ -14,10 +14,10 @@
  * same precision.  Random numbers come from Philox4x32-10 as defined by Salmon,
  * Moraes, Dror and Shaw, "Parallel random numbers: as easy as 1, 2, 3" (SC'11).
  *
- * Readings of points where the paper is silent or garbled (smooth-kNN
- * constants, the union's sign, the schedule, constants gamma = 1, eps = 1e-3,
- * clip 4, the RNG counter layout) are listed in the design notes and are the
- * same on both sides.
+ * Where the paper is silent or garbled (smooth-kNN constants, the union's
+ * sign, the schedule, constants gamma = 1, eps = 1e-3, clip 4, the RNG counter
+ * layout) each function states the reading it takes beside its code; the GPU
+ * library takes the same readings.
  */
 #include <math.h>
 #include <stdint.h>
