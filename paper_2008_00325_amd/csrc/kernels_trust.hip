@@ -43,6 +43,17 @@ __device__ __forceinline__ bool pair_less(float a, int32_t ia, float b, int32_t 
     return a < b || (a == b && ia < ib);
 }
 
+// (distance, index) as one 64-bit key that orders as pair_less does for
+// non-negative indices: the float's bits mapped to an unsigned integer of the
+// same order (negative values flipped whole, positive ones with the sign bit
+// set), -0 first made +0 so that equal floats give equal keys.
+__device__ __forceinline__ uint64_t pair_key(float a, int32_t ia)
+{
+    const uint32_t bits = __float_as_uint(a + 0.0f);
+    const uint32_t ord = (bits & 0x80000000u) ? ~bits : (bits | 0x80000000u);
+    return ((uint64_t)ord << 32) | (uint32_t)ia;
+}
+
 // One wavefront per point i: lanes 0..k-1 hold the k best (distance, index)
 // pairs seen so far, ascending; each chunk of 64 candidates is merged by
 // inserting the qualifying lanes one at a time.
@@ -167,10 +178,10 @@ __device__ __forceinline__ float4 load_features(const float *__restrict__ X, int
 }
 
 template <int KMAX, int CT, int CH>
-__global__ __launch_bounds__(512) void k_tw_rank(const float *__restrict__ X, int64_t n, int32_t d, int32_t k,
-                                                 const float *__restrict__ nx, const int32_t *__restrict__ nbr,
-                                                 const float *__restrict__ thr, int64_t tiles_per_split,
-                                                 int32_t *__restrict__ cnt_out)
+__device__ __forceinline__ void rank_body(const float *__restrict__ X, int64_t n, int32_t d, int32_t k,
+                                          const float *__restrict__ nx, const int32_t *__restrict__ nbr,
+                                          const float *__restrict__ thr, int64_t tiles_per_split,
+                                          int32_t *__restrict__ cnt_out)
 {
     constexpr int COLS = 16 * CT;
     constexpr int PAD = CH + 4;        // floats per staged point
@@ -193,14 +204,14 @@ __global__ __launch_bounds__(512) void k_tw_rank(const float *__restrict__ X, in
     const bool row_ok = row < n;
     const bool vec = (d % 4) == 0 && (reinterpret_cast<uintptr_t>(X) & 15) == 0;   // 16-byte loads
 
-    float th[KMAX];
-    int32_t nb[KMAX];
+    // each threshold as a (distance, index) key; an unused slot gets the
+    // smallest key, which no element is below
+    uint64_t tkey[KMAX];
     int32_t cnt[KMAX];
 #pragma unroll
     for (int s = 0; s < KMAX; ++s) {
         const bool use = row_ok && s < k;
-        th[s] = use ? thr[row * k + s] : -INFINITY;
-        nb[s] = use ? nbr[row * k + s] : -1;
+        tkey[s] = use ? pair_key(thr[row * k + s], nbr[row * k + s]) : 0ull;
         cnt[s] = 0;
     }
     const float nrow = row_ok ? nx[row] : 0.0f;
@@ -277,9 +288,12 @@ __global__ __launch_bounds__(512) void k_tw_rank(const float *__restrict__ X, in
                     if (c >= n || c == row) continue;
                     const float dist = nrow + s_nx[cl] - 2.0f * acc[t][e];
                     const int32_t ci = (int32_t)c;
+                    const uint64_t key = pair_key(dist, ci);
+                    // points ordered before neighbour s, the neighbour itself excluded (its
+                    // distance here need not equal the threshold's bit for bit)
 #pragma unroll
                     for (int s = 0; s < KMAX; ++s)
-                        cnt[s] += (ci != nb[s] && pair_less(dist, ci, th[s], nb[s])) ? 1 : 0;
+                        cnt[s] += (key < tkey[s] && (uint32_t)ci != (uint32_t)tkey[s]) ? 1 : 0;
                 }
             }
         }
@@ -316,6 +330,26 @@ __global__ __launch_bounds__(256) void k_tw_zero(int32_t *__restrict__ p, int64_
     for (int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x; t < count; t += stride) p[t] = 0;
 }
 
+template <int KMAX, int CT, int CH>
+__global__ __launch_bounds__(512) void k_tw_rank(const float *__restrict__ X, int64_t n, int32_t d, int32_t k,
+                                                 const float *__restrict__ nx, const int32_t *__restrict__ nbr,
+                                                 const float *__restrict__ thr, int64_t tiles_per_split,
+                                                 int32_t *__restrict__ cnt_out)
+{
+    rank_body<KMAX, CT, CH>(X, n, d, k, nx, nbr, thr, tiles_per_split, cnt_out);
+}
+
+// The same for k <= 16, held to 128 registers: two blocks per CU, which this
+// instance reaches without spilling (the wider ones would spill).
+template <int KMAX, int CT, int CH>
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4, 8))) void k_tw_rank_occ(
+    const float *__restrict__ X, int64_t n, int32_t d, int32_t k, const float *__restrict__ nx,
+    const int32_t *__restrict__ nbr, const float *__restrict__ thr, int64_t tiles_per_split,
+    int32_t *__restrict__ cnt_out)
+{
+    rank_body<KMAX, CT, CH>(X, n, d, k, nx, nbr, thr, tiles_per_split, cnt_out);
+}
+
 template <int KMAX, int CT, int CH = kRankChunk>
 static void launch_rank(const float *X, int64_t n, int32_t d, int32_t k, const float *nx, const int32_t *nbr,
                         const float *thr, int32_t *cnt, hipStream_t s)
@@ -328,8 +362,12 @@ static void launch_rank(const float *X, int64_t n, int32_t d, int32_t k, const f
     if (splits < 1) splits = 1;
     const int64_t per_split = (n_tiles + splits - 1) / splits;
     splits = (n_tiles + per_split - 1) / per_split;
-    hipLaunchKernelGGL((k_tw_rank<KMAX, CT, CH>), dim3((unsigned)row_blocks, (unsigned)splits), dim3(512), 0, s, X, n,
-                       d, k, nx, nbr, thr, per_split, cnt);
+    if constexpr (KMAX <= 16)
+        hipLaunchKernelGGL((k_tw_rank_occ<KMAX, CT, CH>), dim3((unsigned)row_blocks, (unsigned)splits), dim3(512), 0,
+                           s, X, n, d, k, nx, nbr, thr, per_split, cnt);
+    else
+        hipLaunchKernelGGL((k_tw_rank<KMAX, CT, CH>), dim3((unsigned)row_blocks, (unsigned)splits), dim3(512), 0, s,
+                           X, n, d, k, nx, nbr, thr, per_split, cnt);
 }
 
 // Sum of pen[0..n) in a fixed order: one block, strided partial sums, then a
