@@ -1,0 +1,112 @@
+"""Parity at the limits of the arguments and on degenerate graphs, both
+epoch kernels, against the oracle:
+  * the largest epoch count (2^24 - 1): the fp32 schedule at epochs near 2^24
+    and the step size 1 - n / N down to ~6e-8;
+  * a large neg_rate (100): the general Philox loop and wide record regions;
+  * all weights equal: every kept edge sampled in every epoch;
+  * the smallest graphs: one vertex, one edge pair.
+"""
+
+import sys
+
+import numpy as np
+import pytest
+
+import oracle as O
+from paper_2008_00325_amd import synth
+from paper_2008_00325_amd import umap_layout as U
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-4
+A_DEF, B_DEF = 1.5769434, 0.8950608
+
+
+@pytest.fixture(scope="module", autouse=True)
+def torch_device_first():
+    import torch
+
+    torch.cuda.init()
+    torch.cuda.set_device(0)
+
+
+def case(msg):
+    print(f"[gpu case] {msg}", flush=True)
+    sys.stdout.flush()
+
+
+def _small_graph(n=3001, k=15, seed=3):
+    ids, dist = synth.window_knn(n, k, synth.cluster_bounds(n, 3), seed=seed)
+    return O.fuzzy_graph(ids, dist)
+
+
+def _parity(h, g, E, epochs, N, R, seed, label):
+    for kernel in (0, 1):
+        U.umap_layout_set_kernel(h, kernel)
+        for ep in epochs:
+            case(f"{label} kernel {kernel} epoch {ep}")
+            U.umap_layout_set_embedding(h, E)
+            U.umap_layout_run_epochs(h, seed, ep, ep + 1)
+            ref, act = O.epoch(g, E, ep, A_DEF, B_DEF, N, R, seed)
+            err = float(np.abs(U.umap_layout_get(h).astype(np.float64) - ref).max())
+            st = U.umap_layout_stats(h)
+            print(f"  max|diff| = {err:.3e}  active = {act}", flush=True)
+            assert err <= TOL
+            assert st["active_edges"] == act and st["overflow_redone"] == 0
+
+
+def test_largest_epoch_count():
+    N, R = (1 << 24) - 1, 5
+    r, c, v = _small_graph()
+    n = 3001
+    g = O.prep(n, r, c, v, N)
+    E = synth.embedding_state(n, 2, 4, 10.0)
+    with U.umap_layout_create(n, 2, r, c, v, A_DEF, B_DEF, N, R) as h:
+        assert U.umap_layout_stats(h)["nnz_kept"] == g.nnz
+        for ep in (0, N // 2, N - 2, N - 1):
+            got = U.umap_layout_debug_active(h, ep)
+            assert np.array_equal(got.astype(bool), O.active_mask(g.eps, ep))
+        _parity(h, g, E, (0, N // 2, N - 1), N, R, 8, "N = 2^24 - 1")
+
+
+def test_large_neg_rate():
+    N, R = 30, 100
+    r, c, v = _small_graph(seed=4)
+    n = 3001
+    g = O.prep(n, r, c, v, N)
+    E = synth.embedding_state(n, 3, 5, 10.0)
+    with U.umap_layout_create(n, 3, r, c, v, A_DEF, B_DEF, N, R) as h:
+        _parity(h, g, E, (0, 29), N, R, 9, "neg_rate 100")
+
+
+def test_all_weights_equal():
+    """Every kept edge has eps = 1 and is sampled in every epoch."""
+    N, R = 50, 5
+    r, c, v = _small_graph(seed=5)
+    v = np.ones_like(v)
+    n = 3001
+    g = O.prep(n, r, c, v, N)
+    assert np.all(g.eps == 1.0)
+    E = synth.embedding_state(n, 2, 6, 10.0)
+    with U.umap_layout_create(n, 2, r, c, v, A_DEF, B_DEF, N, R) as h:
+        _parity(h, g, E, (0, 25, 49), N, R, 10, "equal weights")
+        U.umap_layout_run(h, 3)
+        assert U.umap_layout_stats(h)["active_edges"] == g.nnz * N
+
+
+def test_smallest_graphs():
+    # one vertex, no edges: a run is the initial layout
+    with U.umap_layout_create(1, 2, np.zeros(0, np.int32), np.zeros(0, np.int32), np.zeros(0, np.float32),
+                              A_DEF, B_DEF, 10, 5) as h:
+        U.umap_layout_run(h, 7)
+        assert np.array_equal(U.umap_layout_get(h), O.init_layout(1, 2, 7))
+        assert U.umap_layout_stats(h)["active_edges"] == 0
+    # one edge pair: both kernels, every epoch, against the oracle
+    r = np.array([0, 1], np.int32)
+    c = np.array([1, 0], np.int32)
+    v = np.array([0.7, 0.7], np.float32)
+    N, R = 12, 3
+    g = O.prep(2, r, c, v, N)
+    E = np.array([[0.0, 0.0], [3.0, 4.0]], np.float32)
+    with U.umap_layout_create(2, 2, r, c, v, A_DEF, B_DEF, N, R) as h:
+        _parity(h, g, E, range(N), N, R, 11, "one edge pair")
