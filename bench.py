@@ -262,6 +262,40 @@ def trustworthiness_measure(torch, U, n: int = 70_000, d: int = 784, k: int = 15
     }
 
 
+# The paper's trustworthiness times (Table 4: isotropic blobs, 1024 features,
+# k = 15; seconds on one NVIDIA GV100), quoted as context beside ours.
+PAPER_TABLE4_GPU_S = {2000: 0.13, 5000: 0.18, 10000: 0.24, 20000: 0.54, 50000: 2.07, 100000: 5.74}
+
+
+def trustworthiness_sizes(torch, U, sizes=(2000, 5000, 10000, 20000, 50000, 100000), d: int = 1024,
+                          k: int = 15) -> dict:
+    """The GPU trustworthiness at the shapes of the paper's timing table:
+    isotropic blobs (5 centres, std 1) with 1024 features and a random 2-D
+    embedding, host-timed around each blocking call (the best of 3 after one
+    warm-up)."""
+    from paper_2008_00325_amd import synth
+
+    rows = []
+    for n in sizes:
+        X, _ = synth.blobs(n, d, 5, seed=n)
+        Xg = torch.from_numpy(X).cuda()
+        Yg = torch.from_numpy(synth.embedding_state(n, 2, 1)).cuda()
+        U.umap_trustworthiness(Xg, Yg, k)
+        best = float("inf")
+        for _ in range(3):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            U.umap_trustworthiness(Xg, Yg, k)
+            torch.cuda.synchronize()
+            best = min(best, time.perf_counter() - t0)
+        rows.append({"n": n, "s": best, "tflops": 2.0 * n * n * d / best / 1e12,
+                     "paper_gv100_s": PAPER_TABLE4_GPU_S.get(n)})
+        log(f"trustworthiness {n} x {d}: {best * 1e3:.1f} ms (the paper's GV100: {PAPER_TABLE4_GPU_S.get(n)} s)")
+        del Xg, Yg
+    return {"d": d, "k": k, "rows": rows,
+            "note": "the paper's column is its own implementation on an NVIDIA GV100 (context, other hardware)"}
+
+
 def copy_probe(torch, U, mb: int = 1024, reps: int = 5) -> float:
     """HBM copy bandwidth of the library's plain 16-byte copy kernel (GB/s,
     read + write bytes), on the current stream."""
@@ -406,6 +440,7 @@ def main() -> int:
         shard_stats = shard_measure(w, U, (rows, cols, vals), a, b)
         transform_stats = transform_measure(w, U, gpu_steps.layout.cpu().numpy(), a, b)
         trust_stats = trustworthiness_measure(torch, U)
+        trust_stats["paper_table4_shapes"] = trustworthiness_sizes(torch, U)
     copy_gbps = copy_probe(torch, U)
     range_bytes = (w.n * w.dim * 4) // st["table_ranges"]
     table_pow2 = 1 << max(3, (range_bytes - 1).bit_length())
