@@ -87,7 +87,15 @@ def build_input(w, torch, U):
     from paper_2008_00325_amd import synth
 
     t0 = time.time()
-    ids, dist = synth.workload_knn(w)
+    step = 2_000_000
+    mark = [step]
+
+    def progress(rows):
+        if rows >= mark[0]:
+            log(f"kNN lists: {rows} of {w.n} rows ({time.time() - t0:.0f} s)")
+            mark[0] = rows + step
+
+    ids, dist = synth.workload_knn(w, progress if w.n > 4 * step else None)
     log(f"generated kNN lists {ids.shape} in {time.time() - t0:.1f}s")
     n, k = w.n, w.k
     di = torch.from_numpy(ids).cuda()

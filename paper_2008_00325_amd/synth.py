@@ -23,6 +23,8 @@ same shape are used; see the experiments section, dataset table):
 * ``window1m_k30`` as above with k = 30, 100 clusters and a 3-D embedding.
 * ``window5m``    5,000,000 vertices, k = 15, 300 clusters with log-normal
                   (sigma 1) sizes rescaled to sum to n, each at least 129.
+* ``window20m``, ``window50m``  the window1m recipe at 20M and 50M vertices
+                  (600 and 1,500 equal clusters), for measurement at scale.
 """
 
 from __future__ import annotations
@@ -57,6 +59,10 @@ WORKLOADS = {
     "window1m": Workload("window1m", 1_000_000, 15, 2, 200, 5, 0.1, 1.0, 3, "window", 30),
     "window1m_k30": Workload("window1m_k30", 1_000_000, 30, 3, 200, 5, 0.1, 1.0, 4, "window", 100),
     "window5m": Workload("window5m", 5_000_000, 15, 2, 200, 5, 0.1, 1.0, 5, "window", 300),
+    # measurement only (no stored oracle runs): the 2-D table outgrows L2 (20M: 160 MB, inside the 256 MB
+    # Infinity Cache) and then the Infinity Cache too (50M: 400 MB)
+    "window20m": Workload("window20m", 20_000_000, 15, 2, 200, 5, 0.1, 1.0, 8, "window", 600),
+    "window50m": Workload("window50m", 50_000_000, 15, 2, 200, 5, 0.1, 1.0, 9, "window", 1500),
 }
 
 
@@ -100,10 +106,11 @@ def cluster_bounds(n: int, clusters: int, lognormal_sigma: float = 0.0, seed: in
     return np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
 
 
-def window_knn(n: int, k: int, bounds: np.ndarray, seed: int) -> tuple[np.ndarray, np.ndarray]:
+def window_knn(n: int, k: int, bounds: np.ndarray, seed: int, progress=None) -> tuple[np.ndarray, np.ndarray]:
     """Synthetic kNN lists: k distinct neighbours per vertex, drawn uniformly
     without replacement from the +-WINDOW window inside the vertex's cluster.
     Distances are the running sum of k Exp(1) draws, in draw order.
+    `progress(rows_done)`, if given, is called after each block of rows.
 
     Returns ids (n, k) int32 and distances (n, k) float32.
     """
@@ -128,10 +135,12 @@ def window_knn(n: int, k: int, bounds: np.ndarray, seed: int) -> tuple[np.ndarra
         pick = np.take_along_axis(part, order, axis=1)              # draw order
         ids[s:t] = np.take_along_axis(cand, pick, axis=1)
         dist[s:t] = np.cumsum(rng.exponential(1.0, size=(t - s, k)), axis=1)
+        if progress is not None:
+            progress(t)
     return ids, dist
 
 
-def workload_knn(w: Workload) -> tuple[np.ndarray, np.ndarray]:
+def workload_knn(w: Workload, progress=None) -> tuple[np.ndarray, np.ndarray]:
     """kNN ids/distances for a window workload."""
     if w.kind != "window":
         raise ValueError(f"{w.name} needs an exact kNN of its points")
@@ -139,7 +148,7 @@ def workload_knn(w: Workload) -> tuple[np.ndarray, np.ndarray]:
         bounds = cluster_bounds(w.n, w.clusters, lognormal_sigma=1.0, seed=w.seed + 100)
     else:
         bounds = cluster_bounds(w.n, w.clusters)
-    return window_knn(w.n, w.k, bounds, w.seed)
+    return window_knn(w.n, w.k, bounds, w.seed, progress)
 
 
 def workload_points(w: Workload) -> tuple[np.ndarray, np.ndarray]:
