@@ -98,7 +98,7 @@ def test_transform_graph_init_and_epoch_parity():
         assert ei.value.code == U.UMAP_E_INVAL
 
 
-@pytest.mark.parametrize("n_table,dim", [(1_000_000, 2), (400_000, 3)])
+@pytest.mark.parametrize("n_table,dim", [(1_000_000, 2), (400_000, 3), (120_000, 16)])
 def test_transform_epoch_parity_large_table(n_table, dim):
     """A table of several ranges (the negative samples are filed by range):
     50,003 new points with 15 edges each to scattered table rows."""
