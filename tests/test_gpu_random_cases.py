@@ -65,3 +65,82 @@ def test_random_case(case):
             st = U.umap_layout_stats(h)
             assert err <= TOL, (kernel, err)
             assert st["active_edges"] == act and st["overflow_redone"] == 0
+
+
+def _transform_cases(count=12, seed=77):
+    rng = np.random.default_rng(seed)
+    out = []
+    for c in range(count):
+        n_table = int(rng.choice([130, 500, 4096, 20000, 300000]))
+        n_new = int(rng.choice([1, 2, 63, 64, 1000, 7777]))
+        k = int(rng.integers(1, 31))
+        dim = int(rng.integers(1, 17))
+        R = int(rng.integers(0, 13))
+        N = int(rng.choice([1, 3, 50, 100]))
+        out.append((c, n_table, n_new, k, dim, R, N, int(rng.integers(0, N)), int(rng.integers(0, 2**31))))
+    return out
+
+
+@pytest.mark.parametrize("case", _transform_cases(),
+                         ids=lambda c: f"t{c[0]}-table{c[1]}-new{c[2]}-k{c[3]}-dim{c[4]}-R{c[5]}-N{c[6]}")
+def test_random_transform_case(case):
+    """A transform: new points with k scattered edges each into a random
+    frozen table (both kernels)."""
+    c, n_table, n_new, k, dim, R, N, ep, seed = case
+    print(f"[gpu case] random transform {c}: table {n_table} new {n_new} k {k} dim {dim} R {R} N {N} epoch {ep}",
+          flush=True)
+    rng = np.random.default_rng(seed)
+    k = min(k, n_table)
+    rows = np.repeat(np.arange(n_new, dtype=np.int32), k)
+    cols = np.concatenate([rng.choice(n_table, size=k, replace=False) for _ in range(n_new)]).astype(np.int32)
+    vals = rng.uniform(0.01, 1.0, size=rows.size).astype(np.float32)
+    T = synth.embedding_state(n_table, dim, seed % 1000, 10.0)
+    Y = synth.embedding_state(n_new, dim, seed % 997, 10.0)
+    g = O.prep_bipartite(n_new, n_table, rows, cols, vals, N)
+    a, b = A_DEF, B_DEF
+    with U.umap_transform_create(n_new, T, rows, cols, vals, a, b, N, R) as h:
+        for kernel in (0, 1):
+            U.umap_layout_set_kernel(h, kernel)
+            U.umap_layout_set_embedding(h, Y)
+            U.umap_layout_run_epochs(h, seed, ep, ep + 1)
+            ref, act = O.frozen_epoch(g, Y, T, ep, a, b, N, R, seed)
+            err = float(np.abs(U.umap_layout_get(h).astype(np.float64) - ref).max())
+            st = U.umap_layout_stats(h)
+            assert err <= TOL, (kernel, err)
+            assert st["active_edges"] == act and st["overflow_redone"] == 0
+
+
+@pytest.mark.parametrize("case", _cases(12, seed=99), ids=lambda c: f"rows{c[0]}-n{c[1]}-dim{c[3]}-R{c[4]}")
+def test_random_row_range_case(case):
+    """A random row range of a random graph: its rows bit-identical to the
+    whole epoch's, the others unchanged, both within 1e-4 of the oracle."""
+    c, n, deg, dim, R, N, ep, seed = case
+    rng = np.random.default_rng(seed)
+    r0 = int(rng.integers(0, n))
+    r1 = int(rng.integers(r0 + 1, n + 1))
+    print(f"[gpu case] random rows {c}: n {n} rows [{r0}, {r1}) deg {deg} dim {dim} R {R} N {N} epoch {ep}",
+          flush=True)
+    if deg > 0 and n > 1:
+        r, col, v = synth.random_symmetric_coo(n, deg, seed % 100000)
+    else:
+        r = col = np.zeros(0, np.int32)
+        v = np.zeros(0, np.float32)
+    g = O.prep(n, r, col, v, N)
+    E = synth.embedding_state(n, dim, seed % 1000, 10.0)
+    with U.umap_layout_create(n, dim, r, col, v, A_DEF, B_DEF, N, R) as h:
+        for kernel in (0, 1):
+            U.umap_layout_set_kernel(h, kernel)
+            U.umap_layout_set_rows(h, 0, n)
+            U.umap_layout_set_embedding(h, E)
+            U.umap_layout_run_epochs(h, seed, ep, ep + 1)
+            full = U.umap_layout_get(h)
+            U.umap_layout_set_rows(h, r0, r1)
+            U.umap_layout_set_embedding(h, E)
+            U.umap_layout_run_epochs(h, seed, ep, ep + 1)
+            got = U.umap_layout_get(h)
+            assert np.array_equal(got[r0:r1].view(np.uint32), full[r0:r1].view(np.uint32))
+            assert np.array_equal(got[:r0].view(np.uint32), E[:r0].view(np.uint32))
+            assert np.array_equal(got[r1:].view(np.uint32), E[r1:].view(np.uint32))
+            delta = O.epoch_rows(g, E, ep, A_DEF, B_DEF, N, R, seed, np.arange(r0, r1, dtype=np.int64))
+            ref = E[r0:r1].astype(np.float64) + delta
+            assert float(np.abs(got[r0:r1].astype(np.float64) - ref).max()) <= TOL
