@@ -144,3 +144,61 @@ def test_random_row_range_case(case):
             delta = O.epoch_rows(g, E, ep, A_DEF, B_DEF, N, R, seed, np.arange(r0, r1, dtype=np.int64))
             ref = E[r0:r1].astype(np.float64) + delta
             assert float(np.abs(got[r0:r1].astype(np.float64) - ref).max()) <= TOL
+
+
+def _graph_cases(count=8, seed=5150):
+    rng = np.random.default_rng(seed)
+    return [(c, int(rng.choice([2, 17, 300, 4000, 20000])), int(rng.integers(1, 65)), int(rng.integers(0, 2**31)))
+            for c in range(count)]
+
+
+@pytest.mark.parametrize("case", _graph_cases(), ids=lambda c: f"g{c[0]}-n{c[1]}-k{c[2]}")
+def test_random_fuzzy_graph_case(case):
+    """The device fuzzy graph on random kNN lists with the awkward rows: a
+    leading run of zero distances (rho from the first positive one), all-zero
+    rows (sigma floored from the global mean), repeated distances, self ids
+    in some lists (ignored): structure identical to the oracle's union, values
+    within one fp32 ulp."""
+    import torch
+
+    c, n, k, seed = case
+    k = min(k, n - 1) if n > 1 else 1
+    print(f"[gpu case] random fuzzy graph {c}: n {n} k {k}", flush=True)
+    rng = np.random.default_rng(seed)
+    ids = np.empty((n, k), np.int32)
+    for i in range(n):
+        ids[i] = rng.choice(n, size=k, replace=False)
+    dist = np.sort(rng.exponential(1.0, size=(n, k)), axis=1).astype(np.float32)
+    dist = np.round(dist, 1)                                   # repeated values
+    zero_lead = rng.random(n) < 0.2
+    dist[zero_lead, : max(1, k // 3)] = 0.0
+    dist[rng.random(n) < 0.05] = 0.0                           # whole rows at distance 0
+    dist = np.sort(dist, axis=1)
+    di = torch.from_numpy(ids).cuda()
+    dd = torch.from_numpy(dist).cuda()
+    rows = torch.empty(2 * n * k, dtype=torch.int32, device="cuda")
+    cols = torch.empty_like(rows)
+    vals = torch.empty(2 * n * k, dtype=torch.float32, device="cuda")
+    U.umap_fuzzy_graph_device(n, k, di, dd, rows, cols, vals)
+    torch.cuda.synchronize()
+    rg, cg, vg = rows.cpu().numpy(), cols.cpu().numpy(), vals.cpu().numpy()
+    keep = (vg > 0) & (rg != cg)
+    order = np.lexsort((cg[keep], rg[keep]))
+    rg, cg, vg = rg[keep][order], cg[keep][order], vg[keep][order]
+    ro, co, vo = O.fuzzy_union(ids, O.membership(dist, *O.smooth_knn(dist)))
+    vo = vo.astype(np.float32)
+    ko = (vo > 0) & (ro != co)
+    ro, co, vo = ro[ko], co[ko], vo[ko]
+    # rows whose sigma sits on its floor have memberships that underflow; a
+    # value at the edge of fp32's range may be 0 on one side only
+    gpu = dict(zip(zip(rg.tolist(), cg.tolist()), vg.tolist()))
+    ora = dict(zip(zip(ro.tolist(), co.tolist()), vo.tolist()))
+    for key in set(gpu) ^ set(ora):
+        assert gpu.get(key, ora.get(key)) < 1e-30, key
+    both = sorted(set(gpu) & set(ora))
+    a = np.array([gpu[x] for x in both], np.float32)
+    b = np.array([ora[x] for x in both], np.float32)
+    big = (a >= 1e-30) | (b >= 1e-30)
+    ulp = np.abs(a.view(np.int32).astype(np.int64) - b.view(np.int32).astype(np.int64))
+    assert ulp[big].max(initial=0) <= 1
+    assert len(both) > 0.9 * len(ora)
