@@ -202,3 +202,36 @@ def test_random_fuzzy_graph_case(case):
     ulp = np.abs(a.view(np.int32).astype(np.int64) - b.view(np.int32).astype(np.int64))
     assert ulp[big].max(initial=0) <= 1
     assert len(both) > 0.9 * len(ora)
+
+
+def _trust_cases(count=10, seed=31337):
+    rng = np.random.default_rng(seed)
+    out = []
+    for c in range(count):
+        n = int(rng.choice([1000, 2047, 3001, 5000]))
+        k = int(rng.integers(1, 65))
+        while 2 * n - 3 * k - 1 <= 0:
+            k //= 2
+        out.append((c, n, int(rng.integers(1, 101)), int(rng.integers(1, 17)), max(k, 1), int(rng.integers(0, 2**31))))
+    return out
+
+
+@pytest.mark.parametrize("case", _trust_cases(), ids=lambda c: f"tw{c[0]}-n{c[1]}-d{c[2]}-dim{c[3]}-k{c[4]}")
+def test_random_trustworthiness_case(case):
+    """GPU trustworthiness against the oracle's on random shapes: every rank
+    kernel instance (k up to 64), feature counts that are not multiples of 4,
+    embeddings of 1-16 components.  The GPU ranks by fp32 distances (matrix
+    tiles), the oracle by fp64 ones, so a near-tie may be ordered differently;
+    each such swap moves T by 2 / (n k (2n - 3k - 1)), under 2e-8 for n >= 1000
+    (at n = 129, k = 52 one swap alone is 2.95e-6), so the sizes here keep the
+    2e-6 bound many swaps wide."""
+    import torch
+
+    c, n, d, dim, k, seed = case
+    print(f"[gpu case] random trustworthiness {c}: n {n} d {d} dim {dim} k {k}", flush=True)
+    rng = np.random.default_rng(seed)
+    X = rng.standard_normal((n, d)).astype(np.float32)
+    Y = rng.standard_normal((n, dim)).astype(np.float32)
+    got = U.umap_trustworthiness(torch.from_numpy(X).cuda(), torch.from_numpy(Y).cuda(), k)
+    ref = O.trustworthiness(X, Y, k)
+    assert abs(got - ref) <= 2e-6, (got, ref)
