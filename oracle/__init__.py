@@ -301,7 +301,13 @@ def exact_knn(X: np.ndarray, k: int, batch: int = 1024) -> tuple[np.ndarray, np.
         t = min(n, s + batch)
         D = _sqdist(X64[s:t], X64)
         D[np.arange(t - s), np.arange(s, t)] = np.inf
-        cand = np.argpartition(D, k + 1, axis=1)[:, : k + 2]
+        # every point whose (rounded) squared distance is within a relative
+        # 1e-9 of the k-th smallest is a candidate, so that no tie at the k-th
+        # distance (nor a pair the rounding of D misorders) is cut off
+        kth = np.partition(D, k - 1, axis=1)[:, k - 1]
+        cut = kth * (1.0 + 1e-9) + 1e-300
+        width = int((D <= cut[:, None]).sum(axis=1).max())
+        cand = np.argpartition(D, width - 1, axis=1)[:, :width] if width < n else np.tile(np.arange(n), (t - s, 1))
         cd = np.take_along_axis(D, cand, axis=1)
         # exact fp64 distances of the candidates, then order by (distance, index)
         diff = X64[s:t, None, :] - X64[cand]

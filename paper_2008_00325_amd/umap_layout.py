@@ -131,13 +131,30 @@ def _check(rc: int) -> None:
         raise UmapLayoutError(rc, umap_layout_last_error())
 
 
-def _dev(x) -> int | None:
-    """Device address of a torch tensor / raw address."""
+def _dev(x, dtype: str | None = None, count: int = 0, name: str = "array") -> int | None:
+    """Device address of a torch tensor, checked before it reaches the C ABI:
+    a tensor must live on the GPU, be contiguous, hold `dtype` elements
+    ("int32" / "float32"; None: any) and at least `count` of them (for an
+    untyped buffer, `count` bytes), since the library reads or writes exactly
+    that many.  A raw integer address is passed through unchecked (the caller
+    vouches for it).  Raises ValueError."""
     if x is None:
         return None
-    if hasattr(x, "data_ptr"):
-        return int(x.data_ptr())
-    return int(x)
+    if not hasattr(x, "data_ptr"):
+        return int(x)
+    if not getattr(x, "is_cuda", False):
+        raise ValueError(f"{name} must be a GPU tensor, got one on {getattr(x, 'device', '?')}")
+    if not x.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None:
+        got = str(x.dtype).replace("torch.", "")
+        if got != dtype:
+            raise ValueError(f"{name} must hold {dtype}, got {got}")
+        if x.numel() < count:
+            raise ValueError(f"{name} holds {x.numel()} elements, the call needs {count}")
+    elif x.numel() * x.element_size() < count:
+        raise ValueError(f"{name} holds {x.numel() * x.element_size()} bytes, the call needs {count}")
+    return int(x.data_ptr())
 
 
 def _stream(s) -> int | None:
@@ -215,8 +232,13 @@ def umap_transform_create(n_new: int, table, rows, cols, vals, a: float, b: floa
 def umap_layout_create_device(n: int, n_components: int, rows, cols, vals, nnz: int, a: float, b: float,
                               n_epochs: int, neg_rate: int, stream=None) -> Handle:
     out = ctypes.c_void_p()
-    _check(lib().umap_layout_create_device(ctypes.byref(out), n, n_components, _dev(rows), _dev(cols), _dev(vals),
-                                           nnz, a, b, n_epochs, neg_rate, _stream(stream)))
+    if nnz < 0:
+        raise ValueError("nnz must be >= 0")
+    dr = _dev(rows, "int32", nnz, "rows")
+    dc = _dev(cols, "int32", nnz, "cols")
+    dv = _dev(vals, "float32", nnz, "vals")
+    _check(lib().umap_layout_create_device(ctypes.byref(out), n, n_components, dr, dc, dv, nnz, a, b, n_epochs,
+                                           neg_rate, _stream(stream)))
     return Handle(out, n, n_components)
 
 
@@ -239,7 +261,7 @@ def umap_layout_get(h: Handle) -> np.ndarray:
 
 
 def umap_layout_get_device(h: Handle, dev_out) -> None:
-    _check(lib().umap_layout_get_device(h.ptr, _dev(dev_out)))
+    _check(lib().umap_layout_get_device(h.ptr, _dev(dev_out, "float32", h.n * h.dim, "dev_out")))
 
 
 def umap_layout_set_embedding(h: Handle, E: np.ndarray) -> None:
@@ -301,7 +323,10 @@ def umap_layout_debug_negatives(h: Handle, seed: int, epoch: int, e_first: int, 
 
 
 def umap_fuzzy_graph_device(n: int, k: int, knn_ids, knn_dists, rows, cols, vals, stream=None) -> None:
-    _check(lib().umap_fuzzy_graph_device(n, k, _dev(knn_ids), _dev(knn_dists), _dev(rows), _dev(cols), _dev(vals),
+    nk = max(n, 0) * max(k, 0)
+    _check(lib().umap_fuzzy_graph_device(n, k, _dev(knn_ids, "int32", nk, "knn_ids"),
+                                         _dev(knn_dists, "float32", nk, "knn_dists"), _dev(rows, "int32", 2 * nk, "rows"),
+                                         _dev(cols, "int32", 2 * nk, "cols"), _dev(vals, "float32", 2 * nk, "vals"),
                                          _stream(stream)))
 
 
@@ -313,19 +338,24 @@ def umap_fit_ab(spread: float = 1.0, min_dist: float = 0.1) -> tuple[float, floa
 
 
 def umap_probe_copy(src, dst, nbytes: int, stream=None) -> None:
-    _check(lib().umap_probe_copy(_dev(src), _dev(dst), nbytes, _stream(stream)))
+    _check(lib().umap_probe_copy(_dev(src, None, nbytes, "src"), _dev(dst, None, nbytes, "dst"), nbytes,
+                                 _stream(stream)))
 
 
 def umap_trustworthiness(X, Y, k: int, stream=None) -> float:
     """T(k) of embedding Y (n x dim) of points X (n x d); both device tensors (fp32, contiguous)."""
+    if len(X.shape) != 2 or len(Y.shape) != 2:
+        raise ValueError("X and Y must be two-dimensional")
     n, d = int(X.shape[0]), int(X.shape[1])
     dim = int(Y.shape[1])
     if int(Y.shape[0]) != n:
         raise ValueError("X and Y need the same number of rows")
     out = ctypes.c_double()
-    _check(lib().umap_trustworthiness(_dev(X), n, d, _dev(Y), dim, k, ctypes.byref(out), _stream(stream)))
+    _check(lib().umap_trustworthiness(_dev(X, "float32", n * d, "X"), n, d, _dev(Y, "float32", n * dim, "Y"), dim, k,
+                                      ctypes.byref(out), _stream(stream)))
     return out.value
 
 
 def umap_probe_gather(table, entries: int, threads: int, iters: int, out, stream=None) -> None:
-    _check(lib().umap_probe_gather(_dev(table), entries, threads, iters, _dev(out), _stream(stream)))
+    _check(lib().umap_probe_gather(_dev(table, None, 8 * max(entries, 0), "table"), entries, threads, iters,
+                                   _dev(out, None, 4 * max(threads, 0), "out"), _stream(stream)))

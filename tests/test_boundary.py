@@ -167,3 +167,73 @@ def test_create_without_a_gpu_reports_device_error():
     with pytest.raises(U.UmapLayoutError) as ei:
         _create()
     assert ei.value.code == U.UMAP_E_DEVICE
+
+
+# ---------------------------------------------------------------------------
+# the Python binding checks device tensors before they reach the C ABI: a
+# wrong device, layout, dtype or size would be an out-of-bounds device access
+# ---------------------------------------------------------------------------
+
+class _FakeCuda:
+    """Stands in for a GPU tensor on a host without one (the checks read only
+    these attributes; every case below has at least one bad argument, so the
+    library is never called and the null address is never used)."""
+
+    def __init__(self, dtype="float32", numel=16, contiguous=True, itemsize=4, shape=None):
+        import torch
+
+        self.shape = shape if shape is not None else (numel,)
+        self.is_cuda = True
+        self.dtype = getattr(torch, dtype)
+        self._n = numel
+        self._c = contiguous
+        self._s = itemsize
+        self.device = "cuda:0"
+
+    def is_contiguous(self):
+        return self._c
+
+    def numel(self):
+        return self._n
+
+    def element_size(self):
+        return self._s
+
+    def data_ptr(self):
+        return 0
+
+
+def test_binding_rejects_bad_device_tensors():
+    import torch
+
+    h = U.Handle(None, 10, 2)
+    cases = [
+        (lambda: U.umap_layout_get_device(h, torch.zeros(20)), "GPU tensor"),
+        (lambda: U.umap_layout_get_device(h, _FakeCuda("float32", 19)), "needs 20"),
+        (lambda: U.umap_layout_get_device(h, _FakeCuda("float64", 40, itemsize=8)), "float32"),
+        (lambda: U.umap_layout_get_device(h, _FakeCuda("float32", 40, contiguous=False)), "contiguous"),
+        (lambda: U.umap_layout_create_device(10, 2, _FakeCuda("int32", 7), _FakeCuda("int32", 8),
+                                             _FakeCuda("float32", 8), 8, 1.5, 0.9, 10, 5), "rows holds 7"),
+        (lambda: U.umap_layout_create_device(10, 2, _FakeCuda("int32", 8), _FakeCuda("int64", 8, itemsize=8),
+                                             _FakeCuda("float32", 8), 8, 1.5, 0.9, 10, 5), "cols must hold int32"),
+        (lambda: U.umap_layout_create_device(10, 2, _FakeCuda("int32", 8), _FakeCuda("int32", 8),
+                                             torch.zeros(8), 8, 1.5, 0.9, 10, 5), "vals must be a GPU tensor"),
+        (lambda: U.umap_layout_create_device(10, 2, _FakeCuda("int32", 8), _FakeCuda("int32", 8),
+                                             _FakeCuda("float32", 8), -1, 1.5, 0.9, 10, 5), "nnz"),
+        (lambda: U.umap_fuzzy_graph_device(5, 3, _FakeCuda("int32", 15), _FakeCuda("float32", 15),
+                                           _FakeCuda("int32", 30), _FakeCuda("int32", 30), _FakeCuda("float32", 29)),
+         "vals holds 29"),
+        (lambda: U.umap_fuzzy_graph_device(5, 3, _FakeCuda("int32", 14), _FakeCuda("float32", 15),
+                                           _FakeCuda("int32", 30), _FakeCuda("int32", 30), _FakeCuda("float32", 30)),
+         "knn_ids holds 14"),
+        (lambda: U.umap_trustworthiness(_FakeCuda("float32", 11), _FakeCuda("float32", 8), 3), "two-dimensional"),
+        (lambda: U.umap_trustworthiness(_FakeCuda("float32", 39, shape=(10, 4)), _FakeCuda("float32", 20, shape=(10, 2)), 3),
+         "X holds 39"),
+        (lambda: U.umap_probe_copy(_FakeCuda("float32", 3), _FakeCuda("float32", 4), 16), "src holds 12 bytes"),
+        (lambda: U.umap_probe_gather(_FakeCuda("float32", 15), 8, 256, 1, _FakeCuda("float32", 256)),
+         "table holds 60 bytes"),
+    ]
+    for call, frag in cases:
+        with pytest.raises(ValueError) as ei:
+            call()
+        assert frag in str(ei.value), (frag, str(ei.value))
