@@ -109,12 +109,9 @@ __global__ __launch_bounds__(256) void k_epoch_hogwild(EpochArgs A, WaveGraph G)
 
         float diff[DIM], g[DIM], cur[DIM];
         const float d2 = sq_dist<DIM>(yi, yj, diff);
-        const float ca = attraction_coef(d2, A.a, A.b);
+        attraction_grad<DIM>(diff, d2, A.a, A.b, g);
 #pragma unroll
-        for (int d = 0; d < DIM; ++d) {
-            g[d] = clip4(ca * diff[d]);
-            cur[d] = fmaf(alpha, g[d], yi[d]);
-        }
+        for (int d = 0; d < DIM; ++d) cur[d] = fmaf(alpha, g[d], yi[d]);
         auto repel = [&](const float (&y)[DIM]) __attribute__((always_inline)) {
             float df[DIM];
             const float dd = sq_dist<DIM>(cur, y, df);

@@ -83,12 +83,63 @@ __device__ __forceinline__ float pow_b(float d2, float b) { return __builtin_amd
 
 // Attraction: d/dy_i log Phi = c (y_i - y_j), c = -2ab d2^(b-1) / (1 + a d2^b),
 // written as -2ab d2^b / (d2 (1 + a d2^b)) with one hardware reciprocal; 0
-// when the points coincide.  Branch-free (the guard is a select).
+// when the points coincide.  Branch-free (the guard is a select).  Valid for
+// d2 >= kTinyD2 only: below it the hardware logarithm and reciprocal, which
+// take no subnormal input, would turn the product into 0 * inf
+// (attraction_grad handles that range).
+constexpr float kTinyD2 = 0x1p-60f;
 __device__ __forceinline__ float attraction_coef(float d2, float a, float b)
 {
     const float p = pow_b(d2, b);
     const float c = (-2.0f * a * b * p) * __builtin_amdgcn_rcpf(d2 * fmaf(a, p, 1.0f));
     return d2 > 0.0f ? c : 0.0f;
+}
+
+// The clipped attraction of a pair 0 < d2 < kTinyD2 (every component of the
+// difference below 2^-30 in magnitude, d2 possibly subnormal or flushed to 0
+// by the squares).  The difference is scaled by 2^88 (exact), so that its
+// squared norm d2s lies in [2^-122, 2^121] for any nonzero fp32 difference,
+// and each component is evaluated in the log domain:
+//   |c diff_d| = 2ab * q * |diff_d| / d2 = 2^(log2(2ab) + log2 q + 88 + log2(|ds_d| / d2s)),
+//   q = p / (1 + a p), p = d2^b, log2 q = b L - log2(1 + a 2^(b L)), L = log2(d2s) - 176,
+// which neither overflows nor loses p to underflow; the sign is that of -diff_d.
+// Rare by construction (coincident or nearly coincident endpoints), so the
+// extra transcendentals and the IEEE division do not matter.
+template <int DIM>
+__device__ __forceinline__ void attraction_tiny(const float (&diff)[DIM], float a, float b, float (&g)[DIM])
+{
+    constexpr float kS = 0x1p88f;
+    float ds[DIM];
+    float d2s = 0.0f;
+#pragma unroll
+    for (int d = 0; d < DIM; ++d) {
+        ds[d] = diff[d] * kS;
+        d2s = fmaf(ds[d], ds[d], d2s);
+    }
+    const float bl = b * (__builtin_amdgcn_logf(d2s) - 176.0f);
+    const float lq = bl - __builtin_amdgcn_logf(fmaf(a, __builtin_amdgcn_exp2f(bl), 1.0f));
+    const float base = __builtin_amdgcn_logf(2.0f * a * b) + lq + 88.0f;
+#pragma unroll
+    for (int d = 0; d < DIM; ++d) {
+        const float m = __builtin_amdgcn_exp2f(base + __builtin_amdgcn_logf(fabsf(ds[d]) / d2s));
+        g[d] = d2s > 0.0f ? copysignf(fminf(m, kClip), -ds[d]) : 0.0f;
+    }
+}
+
+// Clipped attraction gradient of a pair with difference `diff` (y_i - y_j)
+// and squared distance d2: g_d = clip(c diff_d, -4, 4), 0 when the points
+// coincide (C14 of the readings: the term of a zero distance is 0).
+template <int DIM>
+__device__ __forceinline__ void attraction_grad(const float (&diff)[DIM], float d2, float a, float b, float (&g)[DIM])
+{
+    const float c = attraction_coef(d2, a, b);
+#pragma unroll
+    for (int d = 0; d < DIM; ++d) g[d] = clip4(c * diff[d]);
+    bool tiny = false;
+#pragma unroll
+    for (int d = 0; d < DIM; ++d) tiny |= diff[d] != 0.0f;
+    tiny &= d2 < kTinyD2;
+    if (tiny) attraction_tiny<DIM>(diff, a, b, g);
 }
 
 // Repulsion: d/dy_i log(1 - Phi) = c (y_i - y_k), c = 2b / ((1e-3 + d2)(1 + a d2^b));
@@ -159,11 +210,11 @@ template <int DIM>
 __device__ __forceinline__ void attraction_fixed(const float (&yi)[DIM], const float (&yj)[DIM], float a, float b,
                                                  float mult, long long (&fx)[DIM])
 {
-    float diff[DIM];
+    float diff[DIM], g[DIM];
     const float d2 = sq_dist<DIM>(yi, yj, diff);
-    const float c = attraction_coef(d2, a, b);
+    attraction_grad<DIM>(diff, d2, a, b, g);
 #pragma unroll
-    for (int d = 0; d < DIM; ++d) fx[d] = to_fixed(mult * clip4(c * diff[d]));
+    for (int d = 0; d < DIM; ++d) fx[d] = to_fixed(mult * g[d]);
 }
 
 // Repulsion of vertex i from a negative sample k (callers skip k == i).
