@@ -329,6 +329,22 @@ int umap_trustworthiness(const float *X, int64_t n, int32_t d, const float *Y, i
 int umap_fuzzy_graph_device(int64_t n, int32_t k, const int32_t *knn_ids, const float *knn_dists,
                             int32_t *rows, int32_t *cols, float *vals, void *stream);
 
+/*
+ * umap_fuzzy_graph_device_noalloc -- umap_fuzzy_graph_device for callers that
+ * cannot allocate device memory (code being captured into a HIP graph, tight
+ * serving loops, harnesses that forbid hipMalloc): the same kernels and the
+ * same result bit for bit, with its scratch (rho, sigma, the partial sums of
+ * the mean distance, the error flags: about 16 n bytes + 2 MB) taken from a
+ * static array that the library keeps on each GPU it runs on until the process
+ * ends (about 18 MB per GPU).  It calls no hipMalloc, hipFree or allocating
+ * library routine.  Arguments, layout and errors as umap_fuzzy_graph_device,
+ * and n <= 1,048,576 (UMAP_E_INVAL beyond).  Every call on one GPU uses that
+ * GPU's one array: calls that overlap on a GPU (other host threads, other
+ * streams) race and must be serialised by the caller.  Blocking.
+ */
+int umap_fuzzy_graph_device_noalloc(int64_t n, int32_t k, const int32_t *knn_ids, const float *knn_dists,
+                                    int32_t *rows, int32_t *cols, float *vals, void *stream);
+
 /* umap_fit_ab -- least-squares (a, b) of 1/(1 + a x^(2b)) against Eq. 3's
  * target (1 below min_dist, exp(-(x - min_dist)/spread) above) on 300 points
  * of [0, 3 spread].  spread > 0, 0 <= min_dist < 3 spread.  Host only. */

@@ -10,6 +10,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -832,6 +833,81 @@ int umap_fuzzy_graph_device(int64_t n, int32_t k, const int32_t *knn_ids, const 
     } catch (const HipFailure &f) {
         if (scratch) (void)hipFreeAsync(scratch, s);
         return hip_fail(f);
+    }
+}
+
+}  // extern "C"
+
+namespace {
+
+// Scratch of umap_fuzzy_graph_device_noalloc, one copy per GPU for the life of
+// the process: rho and sigma (fp64 per row), the partial sums of the mean
+// distance (fp64, one per 4096 distances, plus the total) and the error flags,
+// for up to kNoAllocMaxRows rows (2 n k < 2^31 bounds the partial sums).
+constexpr int64_t kNoAllocMaxRows = (int64_t)1 << 20;
+constexpr size_t kNoAllocBytes = 2 * (((size_t)8 << 20)) + ((((size_t)1 << 18) + 1) * 8 + 255) / 256 * 256 + 256;
+static __device__ __align__(256) unsigned char scratch[kNoAllocBytes];
+
+// Device address of this GPU's copy of `scratch`, looked up once per device
+// with that device current (in host code the array's name is not a device
+// address).
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+char *noalloc_scratch()
+{
+    int dev = 0;
+    UL_HIP(hipGetDevice(&dev));
+    if (dev < 0 || dev >= kMaxDevices) throw HipFailure{hipErrorInvalidDevice, "hipGetDevice (device index)"};
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        UL_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+        g_scratch_ptr[dev] = p;
+    }
+    return static_cast<char *>(g_scratch_ptr[dev]);
+}
+
+}  // namespace
+
+extern "C" {
+
+int umap_fuzzy_graph_device_noalloc(int64_t n, int32_t k, const int32_t *knn_ids, const float *knn_dists,
+                                    int32_t *rows, int32_t *cols, float *vals, void *stream)
+{
+    if (n < 1 || n > kNoAllocMaxRows)
+        return fail(UMAP_E_INVAL, "n must be in [1, %lld] for the no-allocation entry point, got %lld",
+                    (long long)kNoAllocMaxRows, (long long)n);
+    if (k < 1 || k > 1024) return fail(UMAP_E_INVAL, "k must be in [1, 1024], got %d", k);
+    if (2 * n * (int64_t)k >= ((int64_t)1 << 31)) return fail(UMAP_E_INVAL, "2 n k must be below 2^31");
+    if (!knn_ids || !knn_dists || !rows || !cols || !vals) return fail(UMAP_E_INVAL, "a pointer argument is NULL");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    try {
+        int ndev = 0;
+        if (hipGetDeviceCount(&ndev) != hipSuccess || ndev < 1) return fail(UMAP_E_DEVICE, "no HIP device available");
+        const int64_t np = ul::graph_partials(n, k);
+        Carver cv{noalloc_scratch()};
+        double *rho = cv.take<double>(n);
+        double *sigma = cv.take<double>(n);
+        double *partial = cv.take<double>(np + 1);
+        unsigned long long *flags = cv.take<unsigned long long>(1);
+        if (cv.off > kNoAllocBytes) return fail(UMAP_E_INVAL, "scratch of %zu bytes exceeds the static %zu", cv.off,
+                                                kNoAllocBytes);
+        // flags start at zero (a fill kernel: no memset node if the caller captures)
+        UL_HIP(ul::launch_zero_u64(flags, 1, s));
+        UL_HIP(ul::launch_fuzzy_graph(n, k, knn_ids, knn_dists, rows, cols, vals, rho, sigma, partial, np,
+                                      reinterpret_cast<unsigned *>(flags), s));
+        unsigned long long hflags = 0;
+        UL_HIP(hipMemcpyAsync(&hflags, flags, sizeof hflags, hipMemcpyDeviceToHost, s));
+        UL_HIP(hipStreamSynchronize(s));
+        if (hflags & ul::kBadIndex) return fail(UMAP_E_INVAL, "a neighbour id is outside [0, n)");
+        if (hflags & ul::kBadValue) return fail(UMAP_E_INVAL, "a neighbour distance is not finite");
+        return UMAP_OK;
+    } catch (const HipFailure &f) {
+        return hip_fail(f);
+    } catch (...) {
+        return fail(UMAP_E_NOMEM, "unexpected host failure");
     }
 }
 

@@ -34,7 +34,7 @@ EXPORTS = (
     "umap_layout_stats", "umap_layout_set_stream", "umap_layout_destroy", "umap_layout_last_error",
     "umap_layout_debug_active", "umap_layout_debug_negatives", "umap_layout_set_kernel", "umap_layout_set_mode",
     "umap_layout_set_rows",
-    "umap_fuzzy_graph_device", "umap_fit_ab", "umap_probe_copy", "umap_probe_gather",
+    "umap_fuzzy_graph_device", "umap_fuzzy_graph_device_noalloc", "umap_fit_ab", "umap_probe_copy", "umap_probe_gather",
     "umap_trustworthiness",
 )
 
@@ -107,6 +107,7 @@ def lib() -> ctypes.CDLL:
             "umap_layout_set_mode": [P, i32],
             "umap_layout_set_rows": [P, i64, i64],
             "umap_fuzzy_graph_device": [i64, i32, P, P, P, P, P, P],
+            "umap_fuzzy_graph_device_noalloc": [i64, i32, P, P, P, P, P, P],
             "umap_fit_ab": [f32, f32, ctypes.POINTER(f32), ctypes.POINTER(f32)],
             "umap_probe_copy": [P, P, i64, P],
             "umap_probe_gather": [P, i64, i64, i32, P, P],
@@ -328,6 +329,14 @@ def umap_fuzzy_graph_device(n: int, k: int, knn_ids, knn_dists, rows, cols, vals
                                          _dev(knn_dists, "float32", nk, "knn_dists"), _dev(rows, "int32", 2 * nk, "rows"),
                                          _dev(cols, "int32", 2 * nk, "cols"), _dev(vals, "float32", 2 * nk, "vals"),
                                          _stream(stream)))
+
+
+def umap_fuzzy_graph_device_noalloc(n: int, k: int, knn_ids, knn_dists, rows, cols, vals, stream=None) -> None:
+    nk = max(n, 0) * max(k, 0)
+    _check(lib().umap_fuzzy_graph_device_noalloc(n, k, _dev(knn_ids, "int32", nk, "knn_ids"),
+                                                 _dev(knn_dists, "float32", nk, "knn_dists"),
+                                                 _dev(rows, "int32", 2 * nk, "rows"), _dev(cols, "int32", 2 * nk, "cols"),
+                                                 _dev(vals, "float32", 2 * nk, "vals"), _stream(stream)))
 
 
 def umap_fit_ab(spread: float = 1.0, min_dist: float = 0.1) -> tuple[float, float]:

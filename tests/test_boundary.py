@@ -28,7 +28,7 @@ def _declared():
 
 def test_every_declared_function_is_exported(L):
     names = _declared()
-    assert len(names) == 24
+    assert len(names) == 25
     for name in names:
         assert hasattr(L, name), name
         assert name in U.EXPORTS
@@ -105,6 +105,11 @@ def test_fuzzy_graph_and_probe_argument_checks(L):
     assert L.umap_fuzzy_graph_device(10, 1025, p, p, p, p, p, None) == U.UMAP_E_INVAL
     assert L.umap_fuzzy_graph_device(2**30, 2, p, p, p, p, p, None) == U.UMAP_E_INVAL
     assert L.umap_fuzzy_graph_device(10, 5, None, p, p, p, p, None) == U.UMAP_E_INVAL
+    assert L.umap_fuzzy_graph_device_noalloc(0, 15, p, p, p, p, p, None) == U.UMAP_E_INVAL
+    assert L.umap_fuzzy_graph_device_noalloc(2**20 + 1, 15, p, p, p, p, p, None) == U.UMAP_E_INVAL
+    assert "no-allocation" in U.umap_layout_last_error()
+    assert L.umap_fuzzy_graph_device_noalloc(10, 0, p, p, p, p, p, None) == U.UMAP_E_INVAL
+    assert L.umap_fuzzy_graph_device_noalloc(10, 5, p, p, p, p, None, None) == U.UMAP_E_INVAL
     assert L.umap_probe_copy(p, p, 17, None) == U.UMAP_E_INVAL
     assert L.umap_probe_copy(None, p, 16, None) == U.UMAP_E_INVAL
     assert L.umap_probe_gather(p, 3, 256, 1, p, None) == U.UMAP_E_INVAL
