@@ -25,6 +25,7 @@ import hashlib
 import json
 import os
 import re
+import subprocess
 import sys
 import time
 
@@ -380,6 +381,31 @@ def gather_probe(torch, U, table_bytes: int, reps: int = 3) -> float:
     return threads * iters * 16 / (ms * 1e-3)
 
 
+def host_cpu() -> dict:
+    """The host the oracle ran on: CPU model, sockets and cores (lscpu), the
+    processor count and the cores this process may use."""
+    info = {"nproc": os.cpu_count(), "usable_cpus": len(os.sched_getaffinity(0))}
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        fields = dict(line.split(":", 1) for line in out.splitlines() if ":" in line)
+        for key, name in (("Model name", "model"), ("Socket(s)", "sockets"), ("Core(s) per socket", "cores_per_socket"),
+                          ("Thread(s) per core", "threads_per_core"), ("CPU max MHz", "max_mhz")):
+            if key in fields:
+                info[name] = fields[key].strip()
+    except (OSError, subprocess.SubprocessError):
+        pass
+    if "model" not in info:
+        try:
+            with open("/proc/cpuinfo") as f:
+                for line in f:
+                    if line.startswith("model name"):
+                        info["model"] = line.split(":", 1)[1].strip()
+                        break
+        except OSError:
+            pass
+    return info
+
+
 def cpu_baseline(w, ids, dist, budget_s: float = 12.0):
     """The C oracle (fp64 push-form Jacobi epochs) timed on the host cores, on
     a sample of epochs spread over the run, from the random initial layout."""
@@ -425,6 +451,7 @@ def cpu_baseline(w, ids, dist, budget_s: float = 12.0):
         "unit": "edge-updates/s",
         "cores": cores,
         "kind": "oracle",
+        "host": host_cpu(),
         "sample": f"{len(done)} of the {w.n_epochs} epochs of the {w.name} layout (spread over the run: "
                   f"{done[:6]}...), each from the random initial layout; fp64 push form, "
                   f"{updates} edge updates in {spent:.2f} s",
@@ -442,9 +469,14 @@ def main() -> int:
     ap.add_argument("--n-components", type=int, default=0,
                     help="embedding dimension in place of the workload's own (same graph)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--extras", action="store_true",
+                    help="also measure the asynchronous mode, one GPU's row share, the transform and the GPU "
+                         "trustworthiness (the rows beyond the layout epochs)")
+    ap.add_argument("--context", action="store_true",
+                    help="also measure the context figures at the shapes of the paper's own experiments (all "
+                         "non-kNN work at 3M points; trustworthiness at the shapes of its timing table)")
     ap.add_argument("--no-extras", action="store_true",
-                    help="skip the asynchronous-mode, transform and trustworthiness figures (profiling runs of "
-                         "the fit's kernels)")
+                    help="the default (kept so that recorded profiling commands stay valid)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (the layout is measured on a single MI355X); got --gpus {args.gpus}",
@@ -480,14 +512,15 @@ def main() -> int:
     launch_ms = epochs_ms / n_epochs
     achieved = bytes_epoch / (launch_ms * 1e-3) / 1e9
     traffic = profiled_traffic(w.name)
-    async_stats = transform_stats = trust_stats = shard_stats = scale_stats = None
-    if not args.no_extras:
-        async_stats = async_mode(w, torch, U, (rows, cols, vals), a, b)
-        shard_stats = shard_measure(w, U, (rows, cols, vals), a, b)
-        scale_stats = non_knn_at_3m(torch, U, a, b)
-        transform_stats = transform_measure(w, U, gpu_steps.layout.cpu().numpy(), a, b)
-        trust_stats = trustworthiness_measure(torch, U)
-        trust_stats["paper_table4_shapes"] = trustworthiness_sizes(torch, U)
+    extras = {}
+    if args.extras and not args.no_extras:
+        extras["async_mode"] = async_mode(w, torch, U, (rows, cols, vals), a, b)
+        extras["row_shares"] = shard_measure(w, U, (rows, cols, vals), a, b)
+        extras["transform"] = transform_measure(w, U, gpu_steps.layout.cpu().numpy(), a, b)
+        extras["trustworthiness"] = trustworthiness_measure(torch, U)
+    if args.context and not args.no_extras:
+        extras["non_knn_at_3m"] = non_knn_at_3m(torch, U, a, b)
+        extras["trustworthiness_paper_table4_shapes"] = trustworthiness_sizes(torch, U)
     copy_gbps = copy_probe(torch, U)
     range_bytes = (w.n * w.dim * 4) // st["table_ranges"]
     table_pow2 = 1 << max(3, (range_bytes - 1).bit_length())
@@ -495,7 +528,8 @@ def main() -> int:
     gather_full = gather_probe(torch, U, 1 << max(3, (w.n * w.dim * 4 - 1).bit_length()))
     # gathers per epoch: a positive sample and neg_rate drawn negatives per sampled edge
     gathers_per_s = st["edge_updates"] / (epochs_ms * 1e-3)
-    gpu_name = torch.cuda.get_device_name(0)
+    props = torch.cuda.get_device_properties(0)
+    gpu_name = f"{props.name} ({getattr(props, 'gcnArchName', '?')}, {props.multi_processor_count} CUs)"
 
     result = {
         "metric": "SGD edge-updates/sec (pos+neg) and 200-epoch layout wall time at 1M points",
@@ -543,9 +577,7 @@ def main() -> int:
                     f"vertex-table range, the slice one repulsion launch gathers from); the probe on the whole "
                     f"{w.n * w.dim * 4 / 1e6:.0f} MB table reaches {gather_full / 1e9:.0f} G/s",
         },
-        **({} if args.no_extras else {"async_mode": async_stats, "row_shares": shard_stats,
-                                       "non_knn_at_3m": scale_stats, "transform": transform_stats,
-                                       "trustworthiness": trust_stats}),
+        **extras,
         "fuzzy_graph_ms": build_input.fuzzy_graph_ms,
         "hbm_copy_probe_GBps": copy_gbps,
         "gpu": gpu_name,

