@@ -9,9 +9,11 @@
 //   3. exclusive scan of the counts -> row_ptr (int64), largest row
 //   4. scatter kept edges into their row's segment (order inside a row is
 //      arbitrary at this point)
-//   5. sort each row by column with a rank sort (the rank of an entry is the
-//      number of smaller columns in its row; equal columns flag a duplicate),
-//      and compute eps = w_max / val
+//   5. sort each row by column, and compute eps = w_max / val: rows of up to
+//      kLongRow entries by a rank sort (the rank of an entry is the number of
+//      smaller columns in its row; equal columns flag a duplicate), longer
+//      rows by a stable radix sort of their columns, one workgroup per row
+//      (equal neighbours after it flag a duplicate)
 //   6. symmetry (not for a bipartite graph): each kept (i, j, v) must find
 //      (j, i) with bit-equal v by binary search in row j
 //   7. wave partition for the epoch kernel
@@ -232,6 +234,12 @@ __global__ __launch_bounds__(256) void k_scatter(const int32_t *__restrict__ row
     }
 }
 
+// Rows longer than this are sorted by k_long_row_sort: the rank sort reads a
+// row once per entry, deg^2 loads in all.
+constexpr int64_t kLongRow = 2048;
+constexpr int kSortThreads = 1024;
+constexpr int kSortWaves = kSortThreads / 64;
+
 __global__ __launch_bounds__(256) void k_row_sort(const int32_t *__restrict__ trow, const int32_t *__restrict__ tcol,
                                                   const float *__restrict__ tval, const int64_t *__restrict__ row_ptr,
                                                   int64_t n, PrepScalars *S, int32_t *__restrict__ col,
@@ -245,6 +253,7 @@ __global__ __launch_bounds__(256) void k_row_sort(const int32_t *__restrict__ tr
         const int32_t r = trow[p];
         const int32_t c = tcol[p];
         const int64_t rs = row_ptr[r], re = row_ptr[r + 1];
+        if (re - rs > kLongRow) continue;   // k_long_row_sort
         // rank of c in its row; eight loads of the row in flight at a time
         int64_t rank = 0;
         for (int64_t q0 = rs; q0 < re; q0 += 8) {
@@ -265,6 +274,103 @@ __global__ __launch_bounds__(256) void k_row_sort(const int32_t *__restrict__ tr
     }
     flags = wave_or(flags);
     if ((threadIdx.x & 63) == 0 && flags) atomicOr(&S->flags, flags);
+}
+
+// list[] = the rows longer than kLongRow, count[0] = how many (zeroed before).
+__global__ __launch_bounds__(256) void k_long_rows(const int64_t *__restrict__ row_ptr, int64_t n,
+                                                   int32_t *__restrict__ list, int32_t *count)
+{
+    const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (r < n && row_ptr[r + 1] - row_ptr[r] > kLongRow) list[atomicAdd(count, 1)] = (int32_t)r;
+}
+
+// One workgroup per long row: a least-significant-digit radix sort of the
+// row's (column, slot) pairs by column, 4-bit digits, each pass stable (the
+// digit's global offset from a counting sweep, then chunks of 1024 entries in
+// order, each entry placed after the earlier entries of its digit: rank in
+// its wavefront by ballot, wavefront offsets in LDS).  The pairs move between
+// two buffers inside the row's own segment: (tcol, sval) and (col, eps) --
+// sval and eps hold the slot as an int until the last step writes them.  An
+// even number of passes leaves the result in (tcol, sval); then col, sval and
+// eps are written in sorted order and equal neighbours flag a duplicate.
+__global__ __launch_bounds__(kSortThreads) void k_long_row_sort(int32_t *__restrict__ tcol,
+                                                                const float *__restrict__ tval,
+                                                                const int64_t *__restrict__ row_ptr,
+                                                                const int32_t *__restrict__ list,
+                                                                const int32_t *__restrict__ count, int32_t passes,
+                                                                PrepScalars *S, int32_t *__restrict__ col,
+                                                                float *__restrict__ sval, float *__restrict__ eps)
+{
+    if ((int32_t)blockIdx.x >= *count) return;
+    __shared__ int32_t s_hist[16];
+    __shared__ int32_t s_wcnt[kSortWaves][16];
+    __shared__ int32_t s_woff[kSortWaves][16];
+    const int32_t r = list[blockIdx.x];
+    const int64_t rs = row_ptr[r], L = row_ptr[r + 1] - rs;
+    const int tid = threadIdx.x, wv = tid / 64, lane = tid % 64;
+    int32_t *const key[2] = {tcol + rs, col + rs};
+    int32_t *const idx[2] = {reinterpret_cast<int32_t *>(sval) + rs, reinterpret_cast<int32_t *>(eps) + rs};
+    for (int64_t t = tid; t < L; t += kSortThreads) idx[0][t] = (int32_t)t;
+    __syncthreads();
+    for (int32_t pass = 0; pass < passes; ++pass) {
+        const int src = pass & 1, dst = src ^ 1;
+        const int shift = 4 * pass;
+        if (tid < 16) s_hist[tid] = 0;
+        __syncthreads();
+        for (int64_t t = tid; t < L; t += kSortThreads) atomicAdd(&s_hist[((uint32_t)key[src][t] >> shift) & 15u], 1);
+        __syncthreads();
+        if (tid == 0) {
+            int32_t run = 0;
+            for (int d = 0; d < 16; ++d) {
+                const int32_t c = s_hist[d];
+                s_hist[d] = run;   // first slot of digit d
+                run += c;
+            }
+        }
+        __syncthreads();
+        for (int64_t c0 = 0; c0 < L; c0 += kSortThreads) {
+            const int64_t t = c0 + tid;
+            const bool valid = t < L;
+            const int32_t k = valid ? key[src][t] : 0;
+            const int32_t ix = valid ? idx[src][t] : 0;
+            const int d = valid ? (int)(((uint32_t)k >> shift) & 15u) : 16;
+            int rank = 0;
+            for (int v = 0; v < 16; ++v) {
+                const unsigned long long m = __ballot(d == v);
+                if (d == v) rank = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+                if (lane == 0) s_wcnt[wv][v] = __popcll(m);
+            }
+            __syncthreads();
+            if (tid < 16) {
+                int32_t run = s_hist[tid];
+                for (int w = 0; w < kSortWaves; ++w) {
+                    s_woff[w][tid] = run;
+                    run += s_wcnt[w][tid];
+                }
+                s_hist[tid] = run;
+            }
+            __syncthreads();
+            if (valid) {
+                const int32_t pos = s_woff[wv][d] + rank;
+                key[dst][pos] = k;
+                idx[dst][pos] = ix;
+            }
+            __syncthreads();
+        }
+    }
+    const float w_max = __uint_as_float(S->wmax_bits);
+    unsigned flags = 0;
+    for (int64_t t = tid; t < L; t += kSortThreads) {
+        const int32_t c = key[0][t];
+        const int32_t ix = idx[0][t];
+        if (t > 0 && key[0][t - 1] == c) flags |= kDuplicate;
+        const float v = tval[rs + ix];
+        col[rs + t] = c;
+        sval[rs + t] = v;
+        eps[rs + t] = w_max / v;
+    }
+    flags = wave_or(flags);
+    if (lane == 0 && flags) atomicOr(&S->flags, flags);
 }
 
 __global__ __launch_bounds__(256) void k_symmetry(const int32_t *__restrict__ trow, const int32_t *__restrict__ col,
@@ -323,6 +429,21 @@ hipError_t launch_prep(const PrepBuffers &B, hipStream_t s)
                        B.scalars, B.row_ptr, B.cursor, B.trow, B.tcol, B.tval);
     hipLaunchKernelGGL(k_row_sort, dim3((unsigned)g), dim3(256), 0, s, B.trow, B.tcol, B.tval, B.row_ptr, B.n,
                        B.scalars, B.col, B.sval, B.eps);
+    // rows longer than kLongRow: their list in deg (free after the scan), its
+    // length in cursor[0] (free after the scatter)
+    const int64_t max_long = B.nnz / (kLongRow + 1);
+    if (max_long > 0) {
+        int32_t passes = 0;   // 4-bit digits of the largest column, rounded up to an even count
+        for (int64_t top = B.n_cols - 1; top > 0; top >>= 4) ++passes;
+        passes += passes & 1;
+        hipError_t e = hipMemsetAsync(B.cursor, 0, sizeof(int32_t), s);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(k_long_rows, dim3((unsigned)((B.n + 255) / 256)), dim3(256), 0, s, B.row_ptr, B.n, B.deg,
+                           B.cursor);
+        const int64_t rows = max_long < B.n ? max_long : B.n;
+        hipLaunchKernelGGL(k_long_row_sort, dim3((unsigned)rows), dim3(kSortThreads), 0, s, B.tcol, B.tval, B.row_ptr,
+                           B.deg, B.cursor, passes, B.scalars, B.col, B.sval, B.eps);
+    }
     if (!B.bipartite)
         hipLaunchKernelGGL(k_symmetry, dim3((unsigned)g), dim3(256), 0, s, B.trow, B.col, B.sval, B.row_ptr, B.n,
                            B.scalars);

@@ -151,6 +151,70 @@ def test_graph_hub_row(n):
                 int(O.active_mask(g.eps, ep).sum()) for ep in range(10))
 
 
+def _stars(n, hubs, seed):
+    """Symmetric COO: each hub h joined to `size` distinct random other
+    vertices (bit-equal values both ways), plus a sparse random graph."""
+    rng = np.random.default_rng(seed)
+    pairs = {}
+    for h, size in hubs:
+        others = rng.choice(np.delete(np.arange(n), h), size=size, replace=False)
+        for j in others:
+            pairs[(min(h, int(j)), max(h, int(j)))] = None
+    r0, c0, _ = synth.random_symmetric_coo(n, 4, seed=seed + 1, shuffle=False)
+    for a, b in zip(r0, c0):
+        if a < b:
+            pairs[(int(a), int(b))] = None
+    lo = np.array([p[0] for p in pairs], np.int32)
+    hi = np.array([p[1] for p in pairs], np.int32)
+    v = (rng.random(lo.size).astype(np.float32) + np.float32(0.01))
+    return np.concatenate([lo, hi]), np.concatenate([hi, lo]), np.concatenate([v, v])
+
+
+def test_graph_long_rows():
+    """Rows longer than the rank sort's limit go through the per-row radix
+    sort: a star whose hub has 2^20 edges ingests bit-exact against the
+    oracle in bounded time (the rank sort would read the hub row 2^40 times),
+    host and device create; hubs of 2,049 to 70,000 edges among ordinary rows;
+    a duplicate inside a long row is reported."""
+    import torch
+
+    n = (1 << 20) + 1
+    others = np.arange(1, n, dtype=np.int32)
+    vals = np.random.default_rng(5).random(n - 1).astype(np.float32) + np.float32(0.01)
+    r = np.concatenate([np.zeros(n - 1, np.int32), others])
+    c = np.concatenate([others, np.zeros(n - 1, np.int32)])
+    v = np.concatenate([vals, vals])
+    r, c, v = _shuffled((r, c, v), 6)
+    g = O.prep(n, r, c, v, 200)
+    case("graph star with a 2^20-edge hub, host create")
+    with U.umap_layout_create(n, 2, r, c, v, A_DEF, B_DEF, 200, 5) as h:
+        _check_graph(h, g)
+        st = U.umap_layout_stats(h)
+        print(f"  ingest {st['prep_ms']:.2f} ms, max degree {st['max_degree']}", flush=True)
+        assert st["max_degree"] == n - 1 and st["prep_ms"] < 500.0
+    case("graph star with a 2^20-edge hub, device create")
+    dr, dc, dv = (torch.from_numpy(x).cuda() for x in (r, c, v))
+    with U.umap_layout_create_device(n, 2, dr, dc, dv, r.size, A_DEF, B_DEF, 200, 5) as h:
+        _check_graph(h, g)
+    n2 = 200_003
+    r, c, v = _stars(n2, [(7, 2075), (100_000, 3000), (199_999, 10_000), (5, 70_000), (6, 2048)], 9)
+    r, c, v = _shuffled((r, c, v), 10)
+    g = O.prep(n2, r, c, v, 50)
+    assert np.diff(g.row_ptr)[7] > 2048 >= np.diff(g.row_ptr)[6]
+    case("graph with hubs of 2,048 to 70,000 edges")
+    with U.umap_layout_create(n2, 3, r, c, v, A_DEF, B_DEF, 50, 5) as h:
+        _check_graph(h, g)
+    case("duplicate inside a long row")
+    # one extra (5, j): only the long row 5 holds a duplicate
+    dup = np.flatnonzero((r == 5) & (c != 6))[:1]
+    r2 = np.concatenate([r, r[dup]])
+    c2 = np.concatenate([c, c[dup]])
+    v2 = np.concatenate([v, v[dup]])
+    with pytest.raises(U.UmapLayoutError) as ei:
+        U.umap_layout_create(n2, 3, r2, c2, v2, A_DEF, B_DEF, 50, 5)
+    assert ei.value.code == U.UMAP_E_INVAL and "more than once" in U.umap_layout_last_error()
+
+
 def test_graph_errors_on_device():
     import torch
 
