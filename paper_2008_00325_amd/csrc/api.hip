@@ -143,6 +143,7 @@ struct umap_layout {
     int cur = 0;
     bool has_layout = false;
     unsigned long long *active = nullptr;   // n_epochs sampled-edge counts
+    unsigned long long *active_sum = nullptr;   // their sum over the last call's epochs
     int32_t *counts = nullptr;              // ring of per-wave counts
     int32_t lg_phases = 0;                  // negative samples split over 2^lg table ranges
     uint32_t *rec = nullptr;                // records of negative samples, slots by record_offset
@@ -208,7 +209,8 @@ int create_common(umap_layout **out, int64_t n, int32_t dim, const int32_t *rows
         const size_t table_elems = table ? (size_t)n_table * (size_t)dim : 0;
         const int64_t n_phases = (int64_t)1 << lg_phases;
         size_t bytes = need<int64_t>(n + 1) + need<int32_t>(nnz) + need<float>(nnz) + need<int32_t>(max_waves + 1) +
-                       2 * need<float>(nd) + need<unsigned long long>(n_epochs) + need<uint8_t>(nnz) +
+                       2 * need<float>(nd) + need<unsigned long long>(n_epochs) + need<unsigned long long>(1) +
+                       need<uint8_t>(nnz) +
                        need<int32_t>((size_t)count_rows * count_stride) +
                        need<uint32_t>(ul::record_offset(max_waves, nnz, neg_rate, (int32_t)n_phases)) +
                        need<int32_t>((size_t)n_phases * max_waves) + need<long long>(nd) + need<unsigned>(1) +
@@ -223,6 +225,7 @@ int create_common(umap_layout **out, int64_t n, int32_t dim, const int32_t *rows
         h->E[0] = cv.take<float>(nd);
         h->E[1] = cv.take<float>(nd);
         h->active = cv.take<unsigned long long>(n_epochs);
+        h->active_sum = cv.take<unsigned long long>(1);
         h->head = cv.take<uint8_t>(nnz);
         h->counts = cv.take<int32_t>((size_t)count_rows * count_stride);
         h->count_stride = count_stride;
@@ -357,10 +360,15 @@ int run_epochs_impl(umap_layout *h, uint64_t seed, int32_t first, int32_t last, 
                     h->delta};
     // the wave kernels store a sample's offset inside its table range and a
     // sampled edge's offset inside its wave in 24 bits (a wave holds fewer
-    // than kWaveCost + max_degree edges); beyond that (n >= 2^28 vertices, or
-    // a row of about 2^24 edges) the one-thread-per-vertex kernel runs
+    // than kWaveCost + max_degree edges), and address a wave's record slots
+    // (1.25 neg_rate x its edges + 256 P) by 32-bit byte offsets; beyond that
+    // (n >= 2^28 vertices, a row of about 2^24 edges, or a huge neg_rate) the
+    // one-thread-per-vertex kernel runs
+    const int64_t wave_slots = (5 * (int64_t)h->neg_rate * ((int64_t)ul::kWaveCost + h->max_degree) + 3) / 4 +
+                               (int64_t)256 * (1 << h->lg_phases) + 1;
     const bool fits = (h->n_table >> h->lg_phases) + 2 < ((int64_t)1 << 24) &&
-                      (int64_t)h->max_degree + ul::kWaveCost < ((int64_t)1 << 24);
+                      (int64_t)h->max_degree + ul::kWaveCost < ((int64_t)1 << 24) &&
+                      wave_slots * (int64_t)sizeof(uint32_t) < ((int64_t)1 << 32);
     const bool async = h->mode == 1;
     if (async && h->table) return fail(UMAP_E_INVAL, "the asynchronous mode applies to fits, not to transforms");
     const bool restricted = h->row_first > 0 || h->row_last < h->n;
@@ -451,12 +459,11 @@ int run_epochs_impl(umap_layout *h, uint64_t seed, int32_t first, int32_t last, 
         }
     }
     UL_HIP(hipEventRecord(h->ev[2], h->stream));
-    std::vector<unsigned long long> act((size_t)h->n_epochs);
-    UL_HIP(hipMemcpyAsync(act.data(), h->active, sizeof(unsigned long long) * h->n_epochs, hipMemcpyDeviceToHost,
-                          h->stream));
-    UL_HIP(hipStreamSynchronize(h->stream));
+    // the call's sampled-edge count, summed on the device (8 bytes come back)
     unsigned long long total = 0;
-    for (int32_t ep = first; ep < last; ++ep) total += act[ep];
+    UL_HIP(ul::launch_sum_u64(h->active + first, last - first, h->active_sum, h->stream));
+    UL_HIP(hipMemcpyAsync(&total, h->active_sum, sizeof total, hipMemcpyDeviceToHost, h->stream));
+    UL_HIP(hipStreamSynchronize(h->stream));
     float ms = 0;
     UL_HIP(hipEventElapsedTime(&ms, h->ev[1], h->ev[2]));
     h->st.epochs_ms = ms;

@@ -144,6 +144,8 @@ int64_t count_slots(int kernel, int64_t n, int64_t n_waves);
 // out[r] = sum of counts[r * stride + 0 .. slots) for r < rows.
 hipError_t launch_reduce_counts(const int32_t *counts, int64_t stride, int64_t slots, int32_t rows,
                                 unsigned long long *out, hipStream_t s);
+// *out = a[0] + ... + a[n - 1].
+hipError_t launch_sum_u64(const unsigned long long *a, int64_t n, unsigned long long *out, hipStream_t s);
 // Epochs whose per-wave counts are kept before they are summed.
 constexpr int kCountRing = 256;
 hipError_t launch_debug_active(const float *eps, int64_t nnz, int32_t epoch, uint8_t *out, hipStream_t s);

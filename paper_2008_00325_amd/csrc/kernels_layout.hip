@@ -210,35 +210,44 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
     if ((int)lane < kMaxPhases) rec_n[lane] = 0;
 
     // ---- classify and compact ----------------------------------------------
+    // The wave's edges are addressed by 32-bit offsets from e0 (fewer than
+    // 2^24 of them) against uniform base pointers.
+    const uint32_t ne = (uint32_t)(e1 - e0);
+    const float *const eps_w = G.eps + e0;
+    const int32_t *const col_w = G.col + e0;
+    const uint8_t *const head_w = G.head + e0;
     int64_t qn = 0;
-    // loads are unconditional (the index is clamped into the wave's range and
+    // loads are unconditional (the offset is clamped into the wave's edges and
     // the value masked) so that the next super-chunk stays in flight
-    auto load_super = [&](int64_t sbase, float (&ev)[kSuper], int32_t (&cv)[kSuper],
+    auto load_super = [&](uint32_t sbase, float (&ev)[kSuper], int32_t (&cv)[kSuper],
                           uint8_t (&hv)[kSuper]) __attribute__((always_inline)) {
 #pragma unroll
         for (int j = 0; j < kSuper; ++j) {
-            int64_t e = sbase + j * kWave + lane;
-            e = e < e1 ? e : e1 - 1;
-            ev[j] = G.eps[e];
-            cv[j] = G.col[e];
-            hv[j] = G.head[e];
+            uint32_t o = sbase + j * kWave + lane;
+            o = o < ne ? o : ne - 1;
+            ev[j] = at32(eps_w, o);
+            cv[j] = at32(col_w, o);
+            hv[j] = at32(head_w, o);
         }
     };
     const int32_t R = A.neg_rate;
     const int32_t lg = G.lg_phases;
     const int64_t roff = record_offset(w, e0, R, G.n_phases);
-    int64_t cap = (record_offset(w + 1, e1, R, G.n_phases) - roff) / G.n_phases;   // slots per range
-    if (G.cap_limit >= 0 && cap > G.cap_limit) cap = G.cap_limit;
+    int64_t cap64 = (record_offset(w + 1, e1, R, G.n_phases) - roff) / G.n_phases;   // slots per range
+    if (G.cap_limit >= 0 && cap64 > G.cap_limit) cap64 = G.cap_limit;
+    // a wave's record slots span less than 2^32 bytes (checked by the host)
+    const uint32_t cap = (uint32_t)cap64;
     uint32_t *const rec_wave = G.rec + roff;   // this wave's slots, range p from p * cap
     uint2 *q = s_q[wv];
     uint32_t qhead = 0, qtail = 0;
+    bool overflow = false;   // a record found its range's slots full
     auto file = [&](uint32_t u, uint32_t i, int h) __attribute__((always_inline)) {
         const uint32_t k = word_to_vertex(u, A.n_table);
         if (FIT && k == i) return;   // a draw equal to the source adds nothing
         const uint32_t p = lg == 0 ? 0u : u >> (32 - lg);
         const uint32_t slot = atomicAdd(&rec_n[p], 1u);
-        if (slot < cap) rec_wave[(int64_t)p * cap + slot] = ((uint32_t)h << 24) | (k - range_base(p, lg, A.n_table));
-        else atomicOr(G.overflow, 1u);
+        if (slot < cap) at32(rec_wave, p * cap + slot) = ((uint32_t)h << 24) | (k - range_base(p, lg, A.n_table));
+        else overflow = true;
     };
     // attraction and negative draws of `count` queued sampled edges
     auto process = [&](int count) __attribute__((always_inline)) {
@@ -284,17 +293,17 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
         }
         qhead += (uint32_t)count;
     };
-    auto scan_super = [&](int64_t sbase, const float (&ev)[kSuper], const int32_t (&cv)[kSuper],
+    auto scan_super = [&](uint32_t sbase, const float (&ev)[kSuper], const int32_t (&cv)[kSuper],
                           const uint8_t (&hv)[kSuper]) __attribute__((always_inline)) {
 #pragma unroll
         for (int j = 0; j < kSuper; ++j) {
-            const int64_t e = sbase + j * kWave + lane;
-            if (sbase + j * kWave >= e1) break;
-            const bool act = edge_active(ev[j], A.epoch) & (e < e1);
+            const uint32_t o = sbase + j * kWave + lane;
+            if (sbase + j * kWave >= ne) break;
+            const bool act = edge_active(ev[j], A.epoch) & (o < ne);
             const unsigned long long m = __ballot(act);
             if (act)
                 q[(qtail + lanes_below(m)) & (kQueue - 1)] =
-                    make_uint2((uint32_t)cv[j], ((uint32_t)hv[j] << 24) | (uint32_t)(e - e0));
+                    make_uint2((uint32_t)cv[j], ((uint32_t)hv[j] << 24) | o);
             const uint32_t nact = (uint32_t)__popcll(m);
             qn += nact;
             qtail += nact;
@@ -306,16 +315,16 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
             } while (qtail - qhead >= (uint32_t)kWave);
         }
     };
-    if (e1 > e0) {
+    if (ne > 0) {
         float ea[kSuper], eb[kSuper];
         int32_t ca[kSuper], cb[kSuper];
         uint8_t ha[kSuper], hb[kSuper];
-        constexpr int64_t kStep = (int64_t)kSuper * kWave;
-        load_super(e0, ea, ca, ha);
-        for (int64_t s0 = e0; s0 < e1; s0 += 2 * kStep) {
+        constexpr uint32_t kStep = (uint32_t)kSuper * kWave;
+        load_super(0, ea, ca, ha);
+        for (uint32_t s0 = 0; s0 < ne; s0 += 2 * kStep) {
             load_super(s0 + kStep, eb, cb, hb);
             scan_super(s0, ea, ca, ha);
-            if (s0 + kStep >= e1) break;
+            if (s0 + kStep >= ne) break;
             load_super(s0 + 2 * kStep, ea, ca, ha);
             scan_super(s0 + kStep, eb, cb, hb);
         }
@@ -335,6 +344,7 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
     // per-wave count, summed by a separate pass (a global atomic per wave on
     // one address would serialise thousands of waves)
     if (lane == 0) A.counts[w] = (int32_t)qn;
+    if (__ballot(overflow) != 0 && lane == 0) atomicOr(G.overflow, 1u);
 }
 
 template <int DIM>
@@ -483,6 +493,26 @@ hipError_t launch_reduce_counts(const int32_t *counts, int64_t stride, int64_t s
 {
     if (rows <= 0) return hipSuccess;
     hipLaunchKernelGGL(k_reduce_counts, dim3((unsigned)rows), dim3(256), 0, s, counts, stride, slots, out);
+    return hipGetLastError();
+}
+
+// *out = a[0] + ... + a[n - 1] (one block; the per-epoch sampled-edge counts of a call)
+__global__ __launch_bounds__(256) void k_sum_u64(const unsigned long long *__restrict__ a, int64_t n,
+                                                 unsigned long long *__restrict__ out)
+{
+    unsigned long long s = 0;
+    for (int64_t t = threadIdx.x; t < n; t += 256) s += a[t];
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
+    __shared__ unsigned long long s_w[4];
+    if ((threadIdx.x & 63) == 0) s_w[threadIdx.x >> 6] = s;
+    __syncthreads();
+    if (threadIdx.x == 0) *out = s_w[0] + s_w[1] + s_w[2] + s_w[3];
+}
+
+hipError_t launch_sum_u64(const unsigned long long *a, int64_t n, unsigned long long *out, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_sum_u64, dim3(1), dim3(256), 0, s, a, n, out);
     return hipGetLastError();
 }
 

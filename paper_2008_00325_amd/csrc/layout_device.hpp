@@ -29,10 +29,16 @@ struct Ctr {
     uint32_t w[4];
 };
 
+// a ^ b ^ c in one v_bitop3_b32 (truth table 0x96)
+__device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t c)
+{
+    return __builtin_amdgcn_bitop3_b32(a, b, c, 0x96);
+}
+
 // Philox4x32 with 10 rounds.  Each round multiplies counter words 0 and 2 by
 // the two round constants (full 64-bit products, one v_mad_u64_u32 each); the
-// high halves are mixed with words 1 and 3 and the round key, and the key
-// advances by the two Weyl increments.
+// high halves are mixed with words 1 and 3 and the round key (one three-input
+// xor each), and the key advances by the two Weyl increments.
 __device__ __forceinline__ Ctr philox4x32_10(Ctr c, uint32_t key_lo, uint32_t key_hi)
 {
 #pragma unroll
@@ -40,9 +46,9 @@ __device__ __forceinline__ Ctr philox4x32_10(Ctr c, uint32_t key_lo, uint32_t ke
         const uint64_t p0 = (uint64_t)0xD2511F53u * c.w[0];
         const uint64_t p1 = (uint64_t)0xCD9E8D57u * c.w[2];
         Ctr nx;
-        nx.w[0] = (uint32_t)(p1 >> 32) ^ c.w[1] ^ key_lo;
+        nx.w[0] = xor3((uint32_t)(p1 >> 32), c.w[1], key_lo);
         nx.w[1] = (uint32_t)p1;
-        nx.w[2] = (uint32_t)(p0 >> 32) ^ c.w[3] ^ key_hi;
+        nx.w[2] = xor3((uint32_t)(p0 >> 32), c.w[3], key_hi);
         nx.w[3] = (uint32_t)p0;
         c = nx;
         key_lo += 0x9E3779B9u;
@@ -180,6 +186,20 @@ __device__ __forceinline__ float sq_dist(const float (&x)[DIM], const float (&y)
         d2 = fmaf(diff[d], diff[d], d2);
     }
     return d2;
+}
+
+// base[i] addressed by a 32-bit byte offset (i * sizeof(T) < 2^32): a
+// uniform base pointer plus one 32-bit register, the SGPR-base form of the
+// global loads and stores.
+template <typename T>
+__device__ __forceinline__ T &at32(T *base, uint32_t i)
+{
+    return *reinterpret_cast<T *>(reinterpret_cast<char *>(base) + (uint32_t)(i * (uint32_t)sizeof(T)));
+}
+template <typename T>
+__device__ __forceinline__ const T &at32(const T *base, uint32_t i)
+{
+    return *reinterpret_cast<const T *>(reinterpret_cast<const char *>(base) + (uint32_t)(i * (uint32_t)sizeof(T)));
 }
 
 template <int DIM>

@@ -13,6 +13,8 @@ oracle on the same seeded inputs:
 
 import sys
 
+import time
+
 import numpy as np
 import pytest
 
@@ -560,12 +562,16 @@ def test_full_run_trustworthiness(blobs_graph):
             U.umap_layout_run(h, seed)
             Eg = U.umap_layout_get(h)
             st = U.umap_layout_stats(h)
+        t0 = time.perf_counter()
         Eo, act = O.run(g, w.dim, a, b, w.n_epochs, w.neg_rate, seed)
+        to_s = time.perf_counter() - t0
         assert st["active_edges"] == int(act.sum())
         assert st["edge_updates"] == int(act.sum()) * (1 + w.neg_rate)
         tg = O.trustworthiness(X, Eg, 15)
         to = O.trustworthiness(X, Eo, 15)
-        print(f"  T(gpu) = {tg:.5f}  T(oracle) = {to:.5f}", flush=True)
+        print(f"  T(gpu) = {tg:.5f}  T(oracle) = {to:.5f}; GPU epochs {st['epochs_ms']:.2f} ms "
+              f"({st['edge_updates'] / (st['epochs_ms'] * 1e-3):.3e} edge-updates/s), oracle run {to_s:.2f} s "
+              f"on {O.num_threads()} threads", flush=True)
         assert abs(tg - to) <= 0.01
         assert np.all(np.isfinite(Eg))
 
@@ -820,7 +826,9 @@ def test_full_run_trustworthiness_image70k():
         Ea = U.umap_layout_get(h)
         sta = U.umap_layout_stats(h)
     case("image70k: oracle layout")
+    t0 = time.perf_counter()
     Eo, act = O.run(g, w.dim, a, b, w.n_epochs, w.neg_rate, seed)
+    to_s = time.perf_counter() - t0
     assert st["active_edges"] == int(act.sum()) == sta["active_edges"]
     assert np.all(np.isfinite(Eg)) and np.all(np.isfinite(Ea))
     case("image70k: trustworthiness of the three layouts")
@@ -828,6 +836,8 @@ def test_full_run_trustworthiness_image70k():
     tg = U.umap_trustworthiness(Xg, torch.from_numpy(Eg).cuda(), 15)
     ta = U.umap_trustworthiness(Xg, torch.from_numpy(Ea).cuda(), 15)
     to = U.umap_trustworthiness(Xg, torch.from_numpy(Eo.astype(np.float32)).cuda(), 15)
-    print(f"  T@15(gpu) = {tg:.5f}  T@15(gpu async) = {ta:.5f}  T@15(oracle) = {to:.5f}", flush=True)
+    print(f"  T@15(gpu) = {tg:.5f}  T@15(gpu async) = {ta:.5f}  T@15(oracle) = {to:.5f}; GPU epochs "
+          f"{st['epochs_ms']:.2f} ms ({st['edge_updates'] / (st['epochs_ms'] * 1e-3):.3e} edge-updates/s), "
+          f"oracle run {to_s:.2f} s on {O.num_threads()} threads", flush=True)
     assert abs(tg - to) <= 0.01
     assert abs(ta - to) <= 0.01
