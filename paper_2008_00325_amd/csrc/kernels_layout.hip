@@ -150,8 +150,9 @@ __global__ __launch_bounds__(256) void k_epoch_rowwise(EpochArgs A, const int64_
 //    range commits the wave's rows of E_{n+1} with coalesced stores.
 // ---------------------------------------------------------------------------
 // The eps / col / head stream is read in super-chunks of kSuper x 64 edges,
-// double buffered in registers: super-chunk s+1 is in flight while s is
-// classified.
+// three deep in registers: super-chunks s+1 and s+2 are in flight while s is
+// classified (the queue only ever holds classified edges, so the depth costs
+// registers, not LDS).
 constexpr int kSuper = 2;
 // Records per lane per step of the repulsion kernel: all of a step's gathers
 // are in flight at once; fewer for wide rows, so that the two DIM-vectors per
@@ -316,17 +317,21 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
         }
     };
     if (ne > 0) {
-        float ea[kSuper], eb[kSuper];
-        int32_t ca[kSuper], cb[kSuper];
-        uint8_t ha[kSuper], hb[kSuper];
+        float ea[kSuper], eb[kSuper], ec[kSuper];
+        int32_t ca[kSuper], cb[kSuper], cc[kSuper];
+        uint8_t ha[kSuper], hb[kSuper], hc[kSuper];
         constexpr uint32_t kStep = (uint32_t)kSuper * kWave;
         load_super(0, ea, ca, ha);
-        for (uint32_t s0 = 0; s0 < ne; s0 += 2 * kStep) {
-            load_super(s0 + kStep, eb, cb, hb);
+        load_super(kStep, eb, cb, hb);
+        for (uint32_t s0 = 0; s0 < ne; s0 += 3 * kStep) {
+            load_super(s0 + 2 * kStep, ec, cc, hc);
             scan_super(s0, ea, ca, ha);
             if (s0 + kStep >= ne) break;
-            load_super(s0 + 2 * kStep, ea, ca, ha);
+            load_super(s0 + 3 * kStep, ea, ca, ha);
             scan_super(s0 + kStep, eb, cb, hb);
+            if (s0 + 2 * kStep >= ne) break;
+            load_super(s0 + 4 * kStep, eb, cb, hb);
+            scan_super(s0 + 2 * kStep, ec, cc, hc);
         }
     }
     if (qtail != qhead) {

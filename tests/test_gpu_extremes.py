@@ -3,6 +3,8 @@ epoch kernels, against the oracle:
   * the largest epoch count (2^24 - 1): the fp32 schedule at epochs near 2^24
     and the step size 1 - n / N down to ~6e-8;
   * a large neg_rate (100): the general Philox loop and wide record regions;
+  * the largest neg_rate (65,535) with a 5,100-edge hub row: a wave's record
+    slots would span more than 4 GB, so the row kernel takes the epochs;
   * all weights equal: every kept edge sampled in every epoch;
   * the smallest graphs: one vertex, one edge pair.
 """
@@ -77,6 +79,30 @@ def test_large_neg_rate():
     E = synth.embedding_state(n, 3, 5, 10.0)
     with U.umap_layout_create(n, 3, r, c, v, A_DEF, B_DEF, N, R) as h:
         _parity(h, g, E, (0, 29), N, R, 9, "neg_rate 100")
+
+
+def test_largest_neg_rate_with_a_hub():
+    """neg_rate 2^16 - 1 and a row of 5,100 edges: the record slots of the
+    hub's wave (1.25 x neg_rate x its edges) pass 4 GB, beyond the 32-bit
+    offsets of the wavefront kernels, so the epochs run on the row kernel
+    (whatever kernel is chosen) and still match the oracle.  The hub's edges
+    have eps in (500, 1000), so a few of them are sampled per epoch; a ring of
+    weight-1 edges among vertices 1..99 is sampled in every epoch."""
+    n, hub, N, R = 5101, 5100, 1000, 65535
+    rng = np.random.default_rng(12)
+    others = np.arange(1, hub + 1, dtype=np.int32)
+    wh = rng.uniform(0.001, 0.002, size=hub).astype(np.float32)
+    ring_a = np.arange(1, 100, dtype=np.int32)
+    ring_b = np.roll(ring_a, -1)
+    r = np.concatenate([np.zeros(hub, np.int32), others, ring_a, ring_b])
+    c = np.concatenate([others, np.zeros(hub, np.int32), ring_b, ring_a])
+    v = np.concatenate([wh, wh, np.ones(2 * ring_a.size, np.float32)])
+    g = O.prep(n, r, c, v, N)
+    assert int(np.diff(g.row_ptr).max()) == hub
+    E = synth.embedding_state(n, 2, 13, 10.0)
+    case("neg_rate 65535, 5,100-edge hub")
+    with U.umap_layout_create(n, 2, r, c, v, A_DEF, B_DEF, N, R) as h:
+        _parity(h, g, E, (700, 701), N, R, 14, "neg_rate 65535 hub")
 
 
 def test_all_weights_equal():
