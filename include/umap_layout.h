@@ -172,6 +172,23 @@ int umap_layout_get_graph(const umap_layout *h, int64_t *row_ptr, int32_t *col, 
 /* umap_layout_stats -- counters and device timings of the handle. */
 int umap_layout_stats(const umap_layout *h, umap_layout_stats_t *out);
 
+/* umap_layout_set_epoch_timing -- enabled != 0: later run / run_epochs calls
+ * record a HIP event on the handle's stream before each of their first
+ * UMAP_MAX_TIMED_EPOCHS epochs and one after the last of them (the events are
+ * created on first use and kept until destroy); 0 turns it off.  Off by
+ * default: an event per epoch costs a few microseconds of launch time. */
+#define UMAP_MAX_TIMED_EPOCHS 4096
+int umap_layout_set_epoch_timing(umap_layout *h, int32_t enabled);
+
+/* umap_layout_epoch_ms -- device time of each timed epoch of the last call
+ * (the time between the events around it, on the handle's stream), in ms, into
+ * out_ms[0 .. min(count, capacity)); returns count >= 0, the epochs the last
+ * call timed (0 when timing was off), or a negative UMAP_E_* code (NULL
+ * handle or out_ms with capacity > 0, capacity < 0).  If the last call's
+ * epochs were redone (stats.overflow_redone), these are the redo's times.
+ * Blocking. */
+int umap_layout_epoch_ms(const umap_layout *h, float *out_ms, int32_t capacity);
+
 /* umap_layout_set_stream -- enqueue later work on `stream` (hipStream_t or
  * NULL).  The caller keeps ownership of the stream and must keep it alive
  * while the handle uses it. */

@@ -153,6 +153,9 @@ struct umap_layout {
     long long *delta = nullptr;             // fixed-point partial sums between launches
     int64_t count_stride = 0;               // slots per ring row
     hipEvent_t ev[3] = {nullptr, nullptr, nullptr};
+    bool time_epochs = false;               // umap_layout_set_epoch_timing
+    std::vector<hipEvent_t> ep_ev;          // per-epoch events (created on first use)
+    int32_t timed = 0;                      // epochs the last call timed
     umap_layout_stats_t st{};
 
     void release()
@@ -160,6 +163,9 @@ struct umap_layout {
         if (stream || arena) (void)hipStreamSynchronize(stream);
         for (auto &e : ev)
             if (e) (void)hipEventDestroy(e);
+        for (auto &e : ep_ev)
+            if (e) (void)hipEventDestroy(e);
+        ep_ev.clear();
         if (arena) (void)hipFree(arena);
         arena = nullptr;
     }
@@ -404,6 +410,18 @@ int run_epochs_impl(umap_layout *h, uint64_t seed, int32_t first, int32_t last, 
     }
     UL_HIP(hipEventRecord(h->ev[1], h->stream));
 
+    // per-epoch events: one before each of the first UMAP_MAX_TIMED_EPOCHS
+    // epochs of the call and one after the last of them
+    h->timed = 0;
+    const int32_t timed = h->time_epochs ? (last - first < UMAP_MAX_TIMED_EPOCHS ? last - first : UMAP_MAX_TIMED_EPOCHS)
+                                         : 0;
+    if (timed > 0) {
+        while ((int32_t)h->ep_ev.size() < timed + 1) {
+            hipEvent_t e = nullptr;
+            UL_HIP(hipEventCreate(&e));
+            h->ep_ev.push_back(e);
+        }
+    }
     // epochs [first, last) with one kernel; fault >= 0 injects a launch error
     auto epochs = [&](int which) -> int {
         UL_HIP(ul::launch_zero_u64(h->active, h->n_epochs, h->stream));
@@ -415,6 +433,7 @@ int run_epochs_impl(umap_layout *h, uint64_t seed, int32_t first, int32_t last, 
                 UL_HIP(hipStreamSynchronize(h->stream));
                 return fail(UMAP_E_DEVICE, "epoch %d launch failed [injected]", ep);
             }
+            if (ep - first < timed) UL_HIP(hipEventRecord(h->ep_ev[(size_t)(ep - first)], h->stream));
             A.epoch = ep;
             A.alpha = 1.0 - (double)ep / (double)h->n_epochs;
             A.counts = h->counts + (int64_t)((ep - pending_from) % ring) * h->count_stride;
@@ -430,6 +449,7 @@ int run_epochs_impl(umap_layout *h, uint64_t seed, int32_t first, int32_t last, 
                 UL_HIP(ul::launch_epoch(which, h->dim, A, G, h->stream));
                 if (!async) h->cur = 1 - h->cur;
             }
+            if (ep + 1 - first == timed) UL_HIP(hipEventRecord(h->ep_ev[(size_t)timed], h->stream));
             if (ep + 1 - pending_from == ring || ep + 1 == last) {
                 UL_HIP(ul::launch_reduce_counts(h->counts, h->count_stride, slots, ep + 1 - pending_from,
                                                 h->active + pending_from, h->stream));
@@ -472,6 +492,7 @@ int run_epochs_impl(umap_layout *h, uint64_t seed, int32_t first, int32_t last, 
         h->st.init_ms = ms;
     }
     h->st.epochs_done = last - first;
+    h->timed = timed;
     h->st.active_edges = (int64_t)total;
     h->st.edge_updates = (int64_t)total * (1 + h->neg_rate);
     return UMAP_OK;
@@ -711,6 +732,28 @@ int umap_layout_set_kernel(umap_layout *h, int32_t which)
     if (which != 0 && which != 1) return fail(UMAP_E_INVAL, "kernel must be 0 or 1, got %d", which);
     h->kernel = which;
     return UMAP_OK;
+}
+
+int umap_layout_set_epoch_timing(umap_layout *h, int32_t enabled)
+{
+    if (!h) return fail(UMAP_E_INVAL, "handle is NULL");
+    h->time_epochs = enabled != 0;
+    return UMAP_OK;
+}
+
+int umap_layout_epoch_ms(const umap_layout *h, float *out_ms, int32_t capacity)
+{
+    if (!h) return fail(UMAP_E_INVAL, "handle is NULL");
+    if (capacity < 0 || (capacity > 0 && !out_ms))
+        return fail(UMAP_E_INVAL, "need capacity >= 0 and out_ms != NULL when capacity > 0");
+    try {
+        const int32_t n = h->timed < capacity ? h->timed : capacity;
+        if (n > 0) UL_HIP(hipEventSynchronize(h->ep_ev[(size_t)n]));
+        for (int32_t i = 0; i < n; ++i) UL_HIP(hipEventElapsedTime(&out_ms[i], h->ep_ev[(size_t)i], h->ep_ev[(size_t)i + 1]));
+        return h->timed;
+    } catch (const HipFailure &f) {
+        return hip_fail(f);
+    }
 }
 
 int umap_layout_set_rows(umap_layout *h, int64_t row_first, int64_t row_last)

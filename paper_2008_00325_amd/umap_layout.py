@@ -26,6 +26,7 @@ UMAP_E_DEVICE = -4
 UMAP_E_STATE = -5
 UMAP_MODE_SYNC = 0
 UMAP_MODE_ASYNC = 1
+UMAP_MAX_TIMED_EPOCHS = 4096
 
 EXPORTS = (
     "umap_layout_create", "umap_layout_create_device", "umap_transform_create", "umap_layout_run",
@@ -33,7 +34,7 @@ EXPORTS = (
     "umap_layout_get", "umap_layout_get_device", "umap_layout_set_embedding", "umap_layout_get_graph",
     "umap_layout_stats", "umap_layout_set_stream", "umap_layout_destroy", "umap_layout_last_error",
     "umap_layout_debug_active", "umap_layout_debug_negatives", "umap_layout_set_kernel", "umap_layout_set_mode",
-    "umap_layout_set_rows",
+    "umap_layout_set_rows", "umap_layout_set_epoch_timing", "umap_layout_epoch_ms",
     "umap_fuzzy_graph_device", "umap_fuzzy_graph_device_noalloc", "umap_fit_ab", "umap_probe_copy", "umap_probe_gather",
     "umap_trustworthiness",
 )
@@ -106,6 +107,8 @@ def lib() -> ctypes.CDLL:
             "umap_layout_set_kernel": [P, i32],
             "umap_layout_set_mode": [P, i32],
             "umap_layout_set_rows": [P, i64, i64],
+            "umap_layout_set_epoch_timing": [P, i32],
+            "umap_layout_epoch_ms": [P, P, i32],
             "umap_fuzzy_graph_device": [i64, i32, P, P, P, P, P, P],
             "umap_fuzzy_graph_device_noalloc": [i64, i32, P, P, P, P, P, P],
             "umap_fit_ab": [f32, f32, ctypes.POINTER(f32), ctypes.POINTER(f32)],
@@ -270,6 +273,20 @@ def umap_layout_set_embedding(h: Handle, E: np.ndarray) -> None:
     if e.shape != (h.n, h.dim):
         raise ValueError(f"embedding must have shape {(h.n, h.dim)}")
     _check(lib().umap_layout_set_embedding(h.ptr, _hp(e)))
+
+
+def umap_layout_set_epoch_timing(h: Handle, enabled: bool) -> None:
+    _check(lib().umap_layout_set_epoch_timing(h.ptr, 1 if enabled else 0))
+
+
+def umap_layout_epoch_ms(h: Handle) -> np.ndarray:
+    """Device ms of each epoch the last call timed (empty when timing was off)."""
+    n = lib().umap_layout_epoch_ms(h.ptr, None, 0)
+    _check(min(n, 0))
+    out = np.empty(max(n, 1), dtype=np.float32)
+    got = lib().umap_layout_epoch_ms(h.ptr, out.ctypes.data, n)
+    _check(min(got, 0))
+    return out[:n]
 
 
 def umap_layout_stats(h: Handle) -> dict:

@@ -28,7 +28,7 @@ def _declared():
 
 def test_every_declared_function_is_exported(L):
     names = _declared()
-    assert len(names) == 25
+    assert len(names) == 27
     for name in names:
         assert hasattr(L, name), name
         assert name in U.EXPORTS
@@ -93,6 +93,8 @@ def test_null_handles_are_rejected(L):
     assert L.umap_layout_set_kernel(None, 0) == U.UMAP_E_INVAL
     assert L.umap_layout_set_mode(None, U.UMAP_MODE_SYNC) == U.UMAP_E_INVAL
     assert L.umap_layout_set_rows(None, 0, 1) == U.UMAP_E_INVAL
+    assert L.umap_layout_set_epoch_timing(None, 1) == U.UMAP_E_INVAL
+    assert L.umap_layout_epoch_ms(None, None, 0) == U.UMAP_E_INVAL
     assert L.umap_layout_debug_active(None, 0, None) == U.UMAP_E_INVAL
     assert L.umap_layout_debug_negatives(None, 0, 0, 0, 0, None) == U.UMAP_E_INVAL
     L.umap_layout_destroy(None)  # no-op

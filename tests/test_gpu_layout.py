@@ -485,6 +485,39 @@ def test_kernels_bit_identical_and_deterministic(window1m_graph):
         assert not np.array_equal(U.umap_layout_get(h), first)
 
 
+def test_epoch_timing(blobs_graph):
+    """Per-epoch HIP events: off by default; on, one device time per epoch of
+    the call whose sum is the call's epochs time, for any kernel; at most 4096
+    epochs of a call are timed; bad arguments are rejected."""
+    w, X, ids, dist, (r, c, v) = blobs_graph
+    case("per-epoch timing, blobs2k")
+    with U.umap_layout_create(w.n, 2, r, c, v, A_DEF, B_DEF, 5000, w.neg_rate) as h:
+        U.umap_layout_init(h, 3)
+        U.umap_layout_run_epochs(h, 3, 0, 10)
+        assert U.umap_layout_epoch_ms(h).size == 0
+        U.umap_layout_set_epoch_timing(h, True)
+        for kernel in (0, 1):
+            U.umap_layout_set_kernel(h, kernel)
+            U.umap_layout_run_epochs(h, 3, 20, 70)
+            t = U.umap_layout_epoch_ms(h)
+            st = U.umap_layout_stats(h)
+            print(f"  kernel {kernel}: 50 epochs {t.sum():.3f} ms (call {st['epochs_ms']:.3f} ms), "
+                  f"min {t.min():.4f} max {t.max():.4f}", flush=True)
+            assert t.size == 50 and np.all(t > 0)
+            assert t.sum() <= st["epochs_ms"] * 1.001 + 1e-3
+            assert t.sum() >= 0.5 * st["epochs_ms"]
+        U.umap_layout_run_epochs(h, 3, 0, 5000)
+        assert U.umap_layout_epoch_ms(h).size == 4096
+        buf = np.zeros(3, np.float32)
+        assert U.lib().umap_layout_epoch_ms(h.ptr, buf.ctypes.data, 3) == 4096
+        assert np.all(buf > 0)
+        assert U.lib().umap_layout_epoch_ms(h.ptr, None, -1) == U.UMAP_E_INVAL
+        assert U.lib().umap_layout_epoch_ms(h.ptr, None, 2) == U.UMAP_E_INVAL
+        U.umap_layout_set_epoch_timing(h, False)
+        U.umap_layout_run_epochs(h, 3, 0, 10)
+        assert U.umap_layout_epoch_ms(h).size == 0
+
+
 def test_two_handles_on_two_streams_in_parallel(window1m_graph):
     """Two host threads, each driving its own handle on its own stream at the
     same time (one with each kernel): every result equals the same run made
