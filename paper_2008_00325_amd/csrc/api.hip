@@ -133,6 +133,8 @@ struct umap_layout {
     void *arena = nullptr;
     int64_t *row_ptr = nullptr;
     int32_t *col = nullptr;
+    int16_t *col16 = nullptr;               // col - row in 16 bits (a fit whose deltas all fit)
+    bool col16_ok = false;
     float *eps = nullptr;
     int32_t *part = nullptr;
     int64_t n_waves = 0;
@@ -214,7 +216,8 @@ int create_common(umap_layout **out, int64_t n, int32_t dim, const int32_t *rows
         const int32_t lg_phases = ul::phase_log2(h->n_table, dim);
         const size_t table_elems = table ? (size_t)n_table * (size_t)dim : 0;
         const int64_t n_phases = (int64_t)1 << lg_phases;
-        size_t bytes = need<int64_t>(n + 1) + need<int32_t>(nnz) + need<float>(nnz) + need<int32_t>(max_waves + 1) +
+        size_t bytes = need<int64_t>(n + 1) + need<int32_t>(nnz) + need<int16_t>(table ? 0 : nnz) + need<float>(nnz) +
+                       need<int32_t>(max_waves + 1) +
                        2 * need<float>(nd) + need<unsigned long long>(n_epochs) + need<unsigned long long>(1) +
                        need<uint8_t>(nnz) +
                        need<int32_t>((size_t)count_rows * count_stride) +
@@ -226,6 +229,7 @@ int create_common(umap_layout **out, int64_t n, int32_t dim, const int32_t *rows
         Carver cv{static_cast<char *>(h->arena)};
         h->row_ptr = cv.take<int64_t>(n + 1);
         h->col = cv.take<int32_t>(nnz);
+        h->col16 = cv.take<int16_t>(table ? 0 : nnz);
         h->eps = cv.take<float>(nnz);
         h->part = cv.take<int32_t>(max_waves + 1);
         h->E[0] = cv.take<float>(nd);
@@ -326,6 +330,15 @@ int create_common(umap_layout **out, int64_t n, int32_t dim, const int32_t *rows
         if (h->n_waves < 1) h->n_waves = 1;
         if (h->n_waves > max_waves) throw HipFailure{hipErrorInvalidValue, "wave count exceeds the arena"};
         UL_HIP(ul::launch_partition(h->row_ptr, 0, n, dim, cost, h->part, h->n_waves, h->head, stream));
+        if (!table && kept > 0) {
+            // a fit's tails as 16-bit offsets from their rows, where they all fit
+            unsigned wide = 1;
+            UL_HIP(hipMemsetAsync(h->overflow, 0, sizeof(unsigned), stream));
+            UL_HIP(ul::launch_col_delta(h->row_ptr, h->col, n, h->col16, h->overflow, stream));
+            UL_HIP(hipMemcpyAsync(&wide, h->overflow, sizeof wide, hipMemcpyDeviceToHost, stream));
+            UL_HIP(hipStreamSynchronize(stream));
+            h->col16_ok = wide == 0;
+        }
         float ms = 0;
         UL_HIP(hipEventElapsedTime(&ms, h->ev[0], h->ev[1]));
         h->st.prep_ms = ms;
@@ -363,7 +376,7 @@ int run_epochs_impl(umap_layout *h, uint64_t seed, int32_t first, int32_t last, 
     ul::WaveGraph G{h->row_ptr,     h->col,       h->eps,    h->head,      h->part,
                     h->n_waves,     1 << h->lg_phases,       h->lg_phases, h->rec,
                     h->rec_count,   h->overflow,  fault_records() ? (int64_t)0 : (int64_t)-1,
-                    h->delta};
+                    h->delta,       h->col16_ok ? h->col16 : nullptr};
     // the wave kernels store a sample's offset inside its table range and a
     // sampled edge's offset inside its wave in 24 bits (a wave holds fewer
     // than kWaveCost + max_degree edges), and address a wave's record slots

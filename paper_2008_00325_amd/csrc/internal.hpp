@@ -87,6 +87,10 @@ hipError_t launch_prep(const PrepBuffers &B, hipStream_t s);
 hipError_t launch_partition(const int64_t *row_ptr, int64_t r0, int64_t r1, int32_t dim, int64_t cost,
                             int32_t *part, int64_t n_waves, uint8_t *head, hipStream_t s);
 hipError_t launch_zero_u64(unsigned long long *p, int64_t count, hipStream_t s);
+// delta[e] = col[e] - row(e) as int16 for the n rows; *wide = 1 (it must start
+// at 0) when some delta needs more than 16 bits.
+hipError_t launch_col_delta(const int64_t *row_ptr, const int32_t *col, int64_t n, int16_t *delta, unsigned *wide,
+                            hipStream_t s);
 
 // ---- layout (kernels_layout.hip) ----
 hipError_t launch_init(float *E, int64_t n, int32_t dim, uint64_t seed, hipStream_t s);
@@ -108,6 +112,7 @@ struct WaveGraph {
     unsigned *overflow;       // set when a record did not fit its range slot
     int64_t cap_limit;        // < 0: none; else record slots per range are cut to it (failure injection)
     long long *delta;         // n x dim fixed-point partial sums between launches
+    const int16_t *col16;     // col - row in 16 bits when every edge's fits (a fit), else null
 };
 
 // First record slot of wave w (edges from e0): every wave gets

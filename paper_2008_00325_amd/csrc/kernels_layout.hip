@@ -173,8 +173,9 @@ __device__ __forceinline__ uint32_t range_base(uint32_t p, int32_t lg, uint32_t 
 
 // FIT: the tails and negatives index the moving layout itself (a fit: halo
 // rows in LDS, self draws skipped, both shares of the attraction); else they
-// index a frozen table (a transform).
-template <int DIM, int NQ, bool FIT>
+// index a frozen table (a transform).  C16: the tails are read as 16-bit
+// offsets from their rows (G.col16), 2 bytes per edge instead of 4.
+template <int DIM, int NQ, bool FIT, bool C16>
 __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
 {
     constexpr int CAP = rows_cap(DIM);
@@ -216,6 +217,7 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
     const uint32_t ne = (uint32_t)(e1 - e0);
     const float *const eps_w = G.eps + e0;
     const int32_t *const col_w = G.col + e0;
+    const int16_t *const col16_w = C16 ? G.col16 + e0 : nullptr;
     const uint8_t *const head_w = G.head + e0;
     int64_t qn = 0;
     // loads are unconditional (the offset is clamped into the wave's edges and
@@ -227,7 +229,10 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
             uint32_t o = sbase + j * kWave + lane;
             o = o < ne ? o : ne - 1;
             ev[j] = at32(eps_w, o);
-            cv[j] = at32(col_w, o);
+            if constexpr (C16)
+                cv[j] = at32(col16_w, o);   // the tail's offset from its row
+            else
+                cv[j] = at32(col_w, o);
             hv[j] = at32(head_w, o);
         }
     };
@@ -302,9 +307,10 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
             if (sbase + j * kWave >= ne) break;
             const bool act = edge_active(ev[j], A.epoch) & (o < ne);
             const unsigned long long m = __ballot(act);
-            if (act)
-                q[(qtail + lanes_below(m)) & (kQueue - 1)] =
-                    make_uint2((uint32_t)cv[j], ((uint32_t)hv[j] << 24) | o);
+            if (act) {
+                const uint32_t tail = C16 ? (uint32_t)((int32_t)r0 + (int32_t)hv[j] + cv[j]) : (uint32_t)cv[j];
+                q[(qtail + lanes_below(m)) & (kQueue - 1)] = make_uint2(tail, ((uint32_t)hv[j] << 24) | o);
+            }
             const uint32_t nact = (uint32_t)__popcll(m);
             qn += nact;
             qtail += nact;
@@ -446,10 +452,19 @@ static hipError_t launch_epoch_dq(int kernel, const EpochArgs &A, const WaveGrap
     }
     const int64_t blocks = (G.n_waves + kWavesPerBlock - 1) / kWavesPerBlock;
     const int64_t grid = ((blocks + 7) / 8) * 8;
+    // the 16-bit tail stream is compiled for the common widths (1-4 components)
+    if constexpr (DIM <= 4) {
+        if (A.same_table && G.col16) {
+            hipLaunchKernelGGL((k_epoch_draw<DIM, NQ, true, true>), dim3((unsigned)grid), dim3(256), 0, s, A, G);
+            for (int32_t p = 0; p < G.n_phases; ++p)
+                hipLaunchKernelGGL((k_epoch_repulse<DIM>), dim3((unsigned)grid), dim3(256), 0, s, A, G, p);
+            return hipGetLastError();
+        }
+    }
     if (A.same_table)
-        hipLaunchKernelGGL((k_epoch_draw<DIM, NQ, true>), dim3((unsigned)grid), dim3(256), 0, s, A, G);
+        hipLaunchKernelGGL((k_epoch_draw<DIM, NQ, true, false>), dim3((unsigned)grid), dim3(256), 0, s, A, G);
     else
-        hipLaunchKernelGGL((k_epoch_draw<DIM, NQ, false>), dim3((unsigned)grid), dim3(256), 0, s, A, G);
+        hipLaunchKernelGGL((k_epoch_draw<DIM, NQ, false, false>), dim3((unsigned)grid), dim3(256), 0, s, A, G);
     for (int32_t p = 0; p < G.n_phases; ++p)
         hipLaunchKernelGGL((k_epoch_repulse<DIM>), dim3((unsigned)grid), dim3(256), 0, s, A, G, p);
     return hipGetLastError();

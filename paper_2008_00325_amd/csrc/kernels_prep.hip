@@ -503,6 +503,31 @@ hipError_t launch_partition(const int64_t *row_ptr, int64_t r0, int64_t r1, int3
     return hipGetLastError();
 }
 
+// delta[e] = col[e] - (row of e) in 16 bits, one thread per row; *wide gets
+// 1 when some delta does not fit (then the wave kernels read the 32-bit
+// columns and delta is not used).
+__global__ void k_col_delta(const int64_t *__restrict__ row_ptr, const int32_t *__restrict__ col, int64_t n,
+                            int16_t *__restrict__ delta, unsigned *__restrict__ wide)
+{
+    const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    bool w = false;
+    if (r < n) {
+        for (int64_t e = row_ptr[r]; e < row_ptr[r + 1]; ++e) {
+            const int64_t d = (int64_t)col[e] - r;
+            w |= d < INT16_MIN || d > INT16_MAX;
+            delta[e] = (int16_t)d;
+        }
+    }
+    if (__ballot(w) != 0 && (threadIdx.x & 63) == 0) atomicOr(wide, 1u);
+}
+
+hipError_t launch_col_delta(const int64_t *row_ptr, const int32_t *col, int64_t n, int16_t *delta, unsigned *wide,
+                            hipStream_t s)
+{
+    hipLaunchKernelGGL(k_col_delta, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, row_ptr, col, n, delta, wide);
+    return hipGetLastError();
+}
+
 __global__ void k_zero_u64(unsigned long long *p, int64_t count)
 {
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
