@@ -164,6 +164,15 @@ constexpr int rep_unroll() { return DIM <= 2 ? 16 : DIM <= 4 ? 8 : DIM <= 8 ? 4 
 // one super-chunk.
 constexpr int kQueue = 256;
 static_assert(kQueue >= kWave - 1 + kSuper * kWave, "queue too small");
+// Halo rows staged on each side of a draw wave: only for 1-2 components.
+// From 3 components on a wave owns fewer rows (86 at 3, 17 at 16) while the
+// halo's LDS grows with the row width, so the halo cost more occupancy than
+// its LDS reads of y_j saved (200 epochs of the 1M window graph, draw kernel
+// with / without: 102.9 / 108.8 us at 2 components, 122.1 / 121.1 at 3,
+// 136.8 / 132.6 at 4, 233.7 / 198.1 at 8, 733.6 / 468.6 at 16).  Without a
+// halo every tail outside the wave's own rows is read from global memory.
+template <int DIM>
+constexpr int draw_halo() { return DIM <= 2 ? kHalo : 0; }
 
 // first vertex of table range p of P = 2^lg (ranges split the 32-bit draw)
 __device__ __forceinline__ uint32_t range_base(uint32_t p, int32_t lg, uint32_t n)
@@ -180,7 +189,9 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
 {
     constexpr int CAP = rows_cap(DIM);
     __shared__ long long s_acc[kWavesPerBlock][CAP * DIM];
-    __shared__ float s_y[kWavesPerBlock][(CAP + 2 * kHalo) * DIM];   // the wave's rows of E_n and halos
+    // a transform's tails index the frozen table: no halo
+    constexpr int kHaloW = FIT ? draw_halo<DIM>() : 0;
+    __shared__ float s_y[kWavesPerBlock][(CAP + 2 * kHaloW) * DIM];   // the wave's rows of E_n and halos
     __shared__ uint32_t s_rec[kWavesPerBlock][kMaxPhases];
     __shared__ uint2 s_q[kWavesPerBlock][kQueue];
 
@@ -199,12 +210,11 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
     const int64_t e1 = uniform64(G.row_ptr[r0 + nrows]);
 
     long long *acc = s_acc[wv];
-    float *yrows = s_y[wv] + kHalo * DIM;   // row h of the wave at yrows[h * DIM], h in [-kHalo, nrows + kHalo)
+    float *yrows = s_y[wv] + kHaloW * DIM;   // row h of the wave at yrows[h * DIM], h in [-kHaloW, nrows + kHaloW)
     uint32_t *rec_n = s_rec[wv];
     const size_t g0 = (size_t)r0 * DIM;
-    // staged rows [lo, hi): the wave's own rows and, when the tails index the
-    // same table, up to kHalo on each side
-    constexpr int64_t halo = FIT ? kHalo : 0;
+    // staged rows [lo, hi): the wave's own rows and up to kHaloW on each side
+    constexpr int64_t halo = kHaloW;
     const int64_t lo = r0 >= halo ? r0 - halo : 0;
     const int64_t hi = r0 + nrows + halo <= (int64_t)A.n ? r0 + nrows + halo : (int64_t)A.n;
     for (int t = lane; t < nrows * DIM; t += kWave) acc[t] = 0;
