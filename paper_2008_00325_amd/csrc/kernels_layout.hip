@@ -173,6 +173,15 @@ static_assert(kQueue >= kWave - 1 + kSuper * kWave, "queue too small");
 // halo every tail outside the wave's own rows is read from global memory.
 template <int DIM>
 constexpr int draw_halo() { return DIM <= 2 ? kHalo : 0; }
+// LDS row stride (in elements) of a wave's int64 sums and fp32 rows.  With an
+// even width of 4 or more components a row is a multiple of 16 bank words, so
+// lanes holding different rows of their wave meet on the same banks; one pad
+// element makes the stride odd and spreads the rows over all banks.
+template <int DIM>
+constexpr int lds_stride() { return DIM >= 4 && DIM % 2 == 0 ? DIM + 1 : DIM; }
+// LDS index of element t of a wave's rows stored back to back (t >= 0)
+template <int DIM, int S>
+__device__ __forceinline__ int lds_at(int t) { if constexpr (S == DIM) return t; else return (t / DIM) * S + t % DIM; }
 
 // first vertex of table range p of P = 2^lg (ranges split the 32-bit draw)
 __device__ __forceinline__ uint32_t range_base(uint32_t p, int32_t lg, uint32_t n)
@@ -188,10 +197,11 @@ template <int DIM, int NQ, bool FIT, bool C16>
 __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
 {
     constexpr int CAP = rows_cap(DIM);
-    __shared__ long long s_acc[kWavesPerBlock][CAP * DIM];
+    constexpr int S = lds_stride<DIM>();
+    __shared__ long long s_acc[kWavesPerBlock][CAP * S];
     // a transform's tails index the frozen table: no halo
     constexpr int kHaloW = FIT ? draw_halo<DIM>() : 0;
-    __shared__ float s_y[kWavesPerBlock][(CAP + 2 * kHaloW) * DIM];   // the wave's rows of E_n and halos
+    __shared__ float s_y[kWavesPerBlock][(CAP + 2 * kHaloW) * S];   // the wave's rows of E_n and halos
     __shared__ uint32_t s_rec[kWavesPerBlock][kMaxPhases];
     __shared__ uint2 s_q[kWavesPerBlock][kQueue];
 
@@ -210,15 +220,20 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
     const int64_t e1 = uniform64(G.row_ptr[r0 + nrows]);
 
     long long *acc = s_acc[wv];
-    float *yrows = s_y[wv] + kHaloW * DIM;   // row h of the wave at yrows[h * DIM], h in [-kHaloW, nrows + kHaloW)
+    float *yrows = s_y[wv] + kHaloW * S;   // row h of the wave at yrows[h * S], h in [-kHaloW, nrows + kHaloW)
     uint32_t *rec_n = s_rec[wv];
     const size_t g0 = (size_t)r0 * DIM;
     // staged rows [lo, hi): the wave's own rows and up to kHaloW on each side
     constexpr int64_t halo = kHaloW;
     const int64_t lo = r0 >= halo ? r0 - halo : 0;
     const int64_t hi = r0 + nrows + halo <= (int64_t)A.n ? r0 + nrows + halo : (int64_t)A.n;
-    for (int t = lane; t < nrows * DIM; t += kWave) acc[t] = 0;
-    for (int64_t t = (lo - r0) * DIM + lane; t < (hi - r0) * DIM; t += kWave) yrows[t] = A.E[(int64_t)g0 + t];
+    for (int t = lane; t < nrows * S; t += kWave) acc[t] = 0;
+    if constexpr (S == DIM) {
+        for (int64_t t = (lo - r0) * DIM + lane; t < (hi - r0) * DIM; t += kWave) yrows[t] = A.E[(int64_t)g0 + t];
+    } else {
+        for (int t = lane; t < (int)(hi - lo) * DIM; t += kWave)
+            yrows[((int)(lo - r0) + t / DIM) * S + t % DIM] = A.E[(int64_t)lo * DIM + t];
+    }
     if ((int)lane < kMaxPhases) rec_n[lane] = 0;
 
     // ---- classify and compact ----------------------------------------------
@@ -275,21 +290,21 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
         const uint32_t i = (uint32_t)(r0 + h);
         float yi[DIM], yj[DIM];
 #pragma unroll
-        for (int d = 0; d < DIM; ++d) yi[d] = yrows[h * DIM + d];
+        for (int d = 0; d < DIM; ++d) yi[d] = yrows[h * S + d];
         // y_j from the staged rows when j is one of them, else from the table;
         // the LDS read is unconditional (a valid row otherwise) so that the
         // two reads never merge into one generic-address load
         const bool near = FIT && (int64_t)tail >= lo && (int64_t)tail < hi;
         const int64_t jt = near ? (int64_t)tail - r0 : 0;
 #pragma unroll
-        for (int d = 0; d < DIM; ++d) yj[d] = yrows[jt * DIM + d];
+        for (int d = 0; d < DIM; ++d) yj[d] = yrows[jt * S + d];
         if (!near) load_row<DIM>(A.T, tail, yj);
         long long fx[DIM];
         attraction_fixed<DIM>(yi, yj, A.a, A.b, FIT ? 2.0f : 1.0f, fx);
         if (valid) {
 #pragma unroll
             for (int d = 0; d < DIM; ++d)
-                atomicAdd(reinterpret_cast<unsigned long long *>(&acc[h * DIM + d]), (unsigned long long)fx[d]);
+                atomicAdd(reinterpret_cast<unsigned long long *>(&acc[h * S + d]), (unsigned long long)fx[d]);
         }
         if (valid) {
             if constexpr (NQ >= 0) {
@@ -357,9 +372,10 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
     wave_sync();
 
     if (A.in_place) {
-        for (int t = lane; t < nrows * DIM; t += kWave) A.E_next[g0 + t] = commit(yrows[t], acc[t], A.alpha);
+        for (int t = lane; t < nrows * DIM; t += kWave)
+            A.E_next[g0 + t] = commit(yrows[lds_at<DIM, S>(t)], acc[lds_at<DIM, S>(t)], A.alpha);
     } else {
-        for (int t = lane; t < nrows * DIM; t += kWave) G.delta[g0 + t] = acc[t];
+        for (int t = lane; t < nrows * DIM; t += kWave) G.delta[g0 + t] = acc[lds_at<DIM, S>(t)];
     }
     if ((int)lane < G.n_phases) G.rec_count[(int64_t)lane * G.n_waves + w] = (int32_t)rec_n[lane];
     // per-wave count, summed by a separate pass (a global atomic per wave on
@@ -372,8 +388,9 @@ template <int DIM>
 __global__ __launch_bounds__(256) void k_epoch_repulse(EpochArgs A, WaveGraph G, int32_t phase)
 {
     constexpr int CAP = rows_cap(DIM);
-    __shared__ long long s_acc[kWavesPerBlock][CAP * DIM];
-    __shared__ float s_y[kWavesPerBlock][CAP * DIM];   // the wave's own rows of E_n
+    constexpr int S = lds_stride<DIM>();
+    __shared__ long long s_acc[kWavesPerBlock][CAP * S];
+    __shared__ float s_y[kWavesPerBlock][CAP * S];   // the wave's own rows of E_n
 
     const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const unsigned lane = threadIdx.x % kWave;
@@ -395,8 +412,8 @@ __global__ __launch_bounds__(256) void k_epoch_repulse(EpochArgs A, WaveGraph G,
     float *yrows = s_y[wv];
     const size_t g0 = (size_t)r0 * DIM;
     for (int t = lane; t < nrows * DIM; t += kWave) {
-        acc[t] = A.in_place ? 0ll : G.delta[g0 + t];
-        yrows[t] = A.E[g0 + t];
+        acc[lds_at<DIM, S>(t)] = A.in_place ? 0ll : G.delta[g0 + t];
+        yrows[lds_at<DIM, S>(t)] = A.E[g0 + t];
     }
     wave_sync();
 
@@ -418,7 +435,7 @@ __global__ __launch_bounds__(256) void k_epoch_repulse(EpochArgs A, WaveGraph G,
         for (int u = 0; u < kRepUnroll; ++u) {
             const int h = (int)(r[u] >> 24);
 #pragma unroll
-            for (int d = 0; d < DIM; ++d) yi[u][d] = yrows[h * DIM + d];
+            for (int d = 0; d < DIM; ++d) yi[u][d] = yrows[h * S + d];
         }
 #pragma unroll
         for (int u = 0; u < kRepUnroll; ++u) {
@@ -428,16 +445,17 @@ __global__ __launch_bounds__(256) void k_epoch_repulse(EpochArgs A, WaveGraph G,
             if (b + u * kWave + lane < nrec) {
 #pragma unroll
                 for (int d = 0; d < DIM; ++d)
-                    atomicAdd(reinterpret_cast<unsigned long long *>(&acc[h * DIM + d]), (unsigned long long)fx[d]);
+                    atomicAdd(reinterpret_cast<unsigned long long *>(&acc[h * S + d]), (unsigned long long)fx[d]);
             }
         }
     }
     wave_sync();
 
     if (last || A.in_place) {
-        for (int t = lane; t < nrows * DIM; t += kWave) A.E_next[g0 + t] = commit(yrows[t], acc[t], A.alpha);
+        for (int t = lane; t < nrows * DIM; t += kWave)
+            A.E_next[g0 + t] = commit(yrows[lds_at<DIM, S>(t)], acc[lds_at<DIM, S>(t)], A.alpha);
     } else {
-        for (int t = lane; t < nrows * DIM; t += kWave) G.delta[g0 + t] = acc[t];
+        for (int t = lane; t < nrows * DIM; t += kWave) G.delta[g0 + t] = acc[lds_at<DIM, S>(t)];
     }
 }
 
