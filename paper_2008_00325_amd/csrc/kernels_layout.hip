@@ -140,7 +140,8 @@ __global__ __launch_bounds__(256) void k_epoch_rowwise(EpochArgs A, const int64_
 //    over the wave's edges, classifies every edge for this epoch and appends
 //    the sampled ones -- compacted with a ballot -- to an LDS ring.  It takes
 //    the ring 64 edges at a time: each lane adds its edge's attraction to the
-//    wave's LDS accumulator (y_j from the staged halo rows when j is near),
+//    wave's LDS accumulator (y_j from the wave's staged rows when j is one
+//    of them or, at 1-2 components, within 64 rows of them),
 //    draws the edge's negative samples and files each one as a 4-byte record
 //    under the range of the vertex table it falls in.  The accumulator goes
 //    to delta.
@@ -189,8 +190,8 @@ __device__ __forceinline__ uint32_t range_base(uint32_t p, int32_t lg, uint32_t 
     return lg == 0 ? 0u : __umulhi(p << (32 - lg), n);
 }
 
-// FIT: the tails and negatives index the moving layout itself (a fit: halo
-// rows in LDS, self draws skipped, both shares of the attraction); else they
+// FIT: the tails and negatives index the moving layout itself (a fit: near
+// tails from LDS, self draws skipped, both shares of the attraction); else they
 // index a frozen table (a transform).  C16: the tails are read as 16-bit
 // offsets from their rows (G.col16), 2 bytes per edge instead of 4.
 template <int DIM, int NQ, bool FIT, bool C16>

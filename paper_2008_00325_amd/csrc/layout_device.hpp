@@ -278,9 +278,10 @@ __device__ __forceinline__ void wave_sync()
 
 // Wavefronts per workgroup of the edge-parallel kernels.
 constexpr int kWavesPerBlock = 4;
-// Rows staged in LDS on each side of a wave's own rows: the attraction reads
-// y_j from there when j is that close (neighbour lists of locally ordered
-// vertices), and from global memory otherwise.
+// Rows staged in LDS on each side of a wave's own rows (by the kernels that
+// stage a halo): the attraction reads y_j from there when j is that close
+// (neighbour lists of locally ordered vertices), and from global memory
+// otherwise.
 constexpr int kHalo = 64;
 
 __device__ __forceinline__ int64_t uniform64(int64_t v)
