@@ -37,6 +37,8 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBPS = 8000.0
 FP32_MFMA_PEAK_TFLOPS = 157.3   # MI355X dense fp32 matrix peak
+# L2 request rate of the chip: 8 XCDs x 16 L2 channels, one 128-byte request per channel per clock at 2.4 GHz
+L2_REQUEST_PEAK_G_PER_S = 8 * 16 * 2.4
 # HBM traffic of one epoch from rocprofv3 FETCH_SIZE / WRITE_SIZE passes (scaled by the
 # same counters on the library's copy probe); valid while the kernel sources hash the same
 PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "epoch_window1m.md")
@@ -82,6 +84,28 @@ def algorithmic_bytes_per_epoch(n: int, dim: int, nnz: int, active: float, neg_r
     kept edge, col of each sampled edge, row_ptr + read y_i + write y_i' per
     vertex, and one dim-vector gather per positive sample and per negative."""
     return 4.0 * nnz + 4.0 * active + (4.0 + 8.0 * dim) * n + 4.0 * dim * active + 4.0 * dim * neg_rate * active
+
+
+def hierarchical_roofline(n: int, dim: int, nnz: int, active: float, neg_rate: int, epoch_us: float) -> dict:
+    """T* = the slowest tier's time for one epoch's algorithmic work at that tier's peak, and T* over the
+    measured epoch: the edge and row streams (the algorithmic bytes without the vertex gathers) against
+    HBM, and every vertex gather (one per sampled edge and per drawn negative, a random line request
+    each) against the L2's request rate."""
+    stream = 4.0 * nnz + 4.0 * active + (4.0 + 8.0 * dim) * n
+    gathers = active * (1.0 + neg_rate)
+    t_hbm = stream / (HBM_PEAK_GBPS * 1e3)                # bytes / (bytes per us)
+    t_l2 = gathers / (L2_REQUEST_PEAK_G_PER_S * 1e3)       # requests / (requests per us)
+    t_star = max(t_hbm, t_l2)
+    return {
+        "t_star_us": t_star,
+        "t_measured_us": epoch_us,
+        "frac": t_star / epoch_us,
+        "bound": "l2-requests" if t_l2 >= t_hbm else "hbm",
+        "tiers": {
+            "hbm": {"bytes": stream, "peak_GBps": HBM_PEAK_GBPS, "t_us": t_hbm},
+            "l2": {"requests": gathers, "peak_G_per_s": L2_REQUEST_PEAK_G_PER_S, "t_us": t_l2},
+        },
+    }
 
 
 def build_input(w, torch, U):
@@ -576,6 +600,12 @@ def main() -> int:
                     f"epochs time, against the library's gather probe on a {table_pow2 >> 20} MB table (one "
                     f"vertex-table range, the slice one repulsion launch gathers from); the probe on the whole "
                     f"{w.n * w.dim * 4 / 1e6:.0f} MB table reaches {gather_full / 1e9:.0f} G/s",
+        },
+        "hierarchical_roofline": {
+            **hierarchical_roofline(w.n, w.dim, st["nnz_kept"], avg_active, w.neg_rate, launch_ms * 1e3),
+            "note": f"L2 request peak from the chip's structure (8 XCDs x 16 channels x 2.4 GHz); the "
+                    f"library's gather probe on a {table_pow2 >> 20} MB table reaches "
+                    f"{gather_range / 1e9 / L2_REQUEST_PEAK_G_PER_S:.2f} of it",
         },
         **extras,
         "fuzzy_graph_ms": build_input.fuzzy_graph_ms,

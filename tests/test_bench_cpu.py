@@ -1,5 +1,5 @@
 """Host logic of bench.py (no GPU): the single-GPU contract, the algorithmic
-bytes of an epoch, and the rule that ties a profile's traffic figure to the
+bytes of an epoch, the tiered roofline, and the rule that ties a profile's traffic figure to the
 kernel sources it was taken on."""
 
 import os
@@ -28,6 +28,20 @@ def test_algorithmic_bytes_by_hand():
     # the 1M-vertex workload's figure: 26,687,328 kept edges, 7,629,883 sampled per epoch on average
     b = bench.algorithmic_bytes_per_epoch(1_000_000, 2, 26_687_328, 7_629_882.92, 5)
     assert abs(b / 1e6 - 523.5) < 0.1
+
+
+def test_hierarchical_roofline_by_hand():
+    # 10 vertices in 2-D, 40 kept edges, 12 sampled, 5 negatives each: streams 160 + 48 + 200 = 408 bytes,
+    # 12 x 6 = 72 vertex gathers; HBM at 8 TB/s = 8e6 bytes per us, L2 at 307.2e3 requests per us
+    r = bench.hierarchical_roofline(10, 2, 40, 12, 5, epoch_us=1.0)
+    assert abs(r["tiers"]["hbm"]["t_us"] - 408 / 8e6) < 1e-15
+    assert abs(r["tiers"]["l2"]["t_us"] - 72 / 307.2e3) < 1e-15
+    assert r["bound"] == "l2-requests" and abs(r["frac"] - 72 / 307.2e3) < 1e-15
+    # the 1M-vertex workload: 157.3 MB of streams (19.7 us), 45.78 M gathers (149.0 us)
+    r = bench.hierarchical_roofline(1_000_000, 2, 26_687_328, 7_629_882.92, 5, epoch_us=306.5)
+    assert abs(r["tiers"]["hbm"]["t_us"] - 19.66) < 0.01
+    assert abs(r["tiers"]["l2"]["t_us"] - 149.02) < 0.01
+    assert abs(r["frac"] - 149.02 / 306.5) < 1e-4
 
 
 def test_kernel_hash_ignores_comments(tmp_path, monkeypatch):
