@@ -461,6 +461,32 @@ def test_single_epoch_dims_and_rates(dim, R, N):
                               f"dim {dim} R {R} kernel {kernel} scale {scale}")
 
 
+@pytest.mark.parametrize("dim", list(range(1, 17)))
+def test_every_width_both_kernels(dim):
+    # every embedding width on a locally ordered graph (all tails within +-64
+    # rows): the wave kernels stage halo rows at 1-2 components and read other
+    # tails from global memory, and pad the LDS rows of even widths from 4 on;
+    # one epoch of each kernel must match the oracle and each other bit for bit
+    n, N, R = 4001, 60, 5
+    print(f"[gpu case] width {dim}", flush=True)
+    ids, dist = synth.window_knn(n, 15, synth.cluster_bounds(n, 2), seed=40 + dim)
+    r, c, v = O.fuzzy_graph(ids, dist)
+    g = O.prep(n, r, c, v, N)
+    E = synth.embedding_state(n, dim, 300 + dim, 10.0)
+    ref, act = O.epoch(g, E, 7, A_DEF, B_DEF, N, R, 11)
+    outs = []
+    with U.umap_layout_create(n, dim, r, c, v, A_DEF, B_DEF, N, R) as h:
+        for kernel in (0, 1):
+            U.umap_layout_set_kernel(h, kernel)
+            U.umap_layout_set_embedding(h, E)
+            U.umap_layout_run_epochs(h, 11, 7, 8)
+            got = U.umap_layout_get(h)
+            assert float(np.abs(got.astype(np.float64) - ref).max()) <= TOL, (dim, kernel)
+            assert U.umap_layout_stats(h)["active_edges"] == act
+            outs.append(got)
+    assert np.array_equal(outs[0].view(np.uint32), outs[1].view(np.uint32)), dim
+
+
 # ---------------------------------------------------------------------------
 # whole runs
 # ---------------------------------------------------------------------------
