@@ -270,6 +270,9 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
     // a wave's record slots span less than 2^32 bytes (checked by the host)
     const uint32_t cap = (uint32_t)cap64;
     uint32_t *const rec_wave = G.rec + roff;   // this wave's slots, range p from p * cap
+    // One table range: the whole table stays in L2 beside the edge stream, so
+    // each negative's repulsion is applied here (no records, no range launch)
+    const bool fused = G.n_phases == 1;
     uint2 *q = s_q[wv];
     uint32_t qhead = 0, qtail = 0;
     bool overflow = false;   // a record found its range's slots full
@@ -280,6 +283,30 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
         const uint32_t slot = atomicAdd(&rec_n[p], 1u);
         if (slot < cap) at32(rec_wave, p * cap + slot) = ((uint32_t)h << 24) | (k - range_base(p, lg, A.n_table));
         else overflow = true;
+    };
+    // repulsions of four drawn words of a lane's edge, applied at once: all
+    // four table rows are loaded before the first term is computed
+    auto repel4 = [&](const uint32_t *u, int cnt, uint32_t i, int h, const float (&yi)[DIM], bool live)
+                      __attribute__((always_inline)) {
+        uint32_t k[4];
+        float yk[4][DIM];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            k[r] = word_to_vertex(u[r], A.n_table);
+            if (r < cnt) load_row<DIM>(A.T, k[r], yk[r]);
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            if (r < cnt) {
+                long long fx[DIM];
+                repulsion_fixed<DIM>(yi, yk[r], A.a, A.b, fx);
+                if (live && !(FIT && k[r] == i)) {
+#pragma unroll
+                    for (int d = 0; d < DIM; ++d)
+                        atomicAdd(reinterpret_cast<unsigned long long *>(&acc[h * S + d]), (unsigned long long)fx[d]);
+                }
+            }
+        }
     };
     // attraction and negative draws of `count` queued sampled edges
     auto process = [&](int count) __attribute__((always_inline)) {
@@ -307,7 +334,13 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
             for (int d = 0; d < DIM; ++d)
                 atomicAdd(reinterpret_cast<unsigned long long *>(&acc[h * S + d]), (unsigned long long)fx[d]);
         }
-        if (valid) {
+        if (fused) {
+            // every lane draws (the words of a lane without an edge add nothing)
+            for (int32_t qq = 0; 4 * qq < R; ++qq) {
+                const Ctr wd = negative_words(e, A.epoch, qq, A.key_lo, A.key_hi);
+                repel4(wd.w, R - 4 * qq, i, h, yi, valid);
+            }
+        } else if (valid) {
             if constexpr (NQ >= 0) {
                 uint32_t u[4 * NQ > 0 ? 4 * NQ : 1];
                 if constexpr (NQ > 0) negative_words_all<NQ>(e, A.epoch, A.key_lo, A.key_hi, u);
@@ -372,7 +405,7 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
     }
     wave_sync();
 
-    if (A.in_place) {
+    if (A.in_place || fused) {
         for (int t = lane; t < nrows * DIM; t += kWave)
             A.E_next[g0 + t] = commit(yrows[lds_at<DIM, S>(t)], acc[lds_at<DIM, S>(t)], A.alpha);
     } else {
@@ -485,7 +518,7 @@ static hipError_t launch_epoch_dq(int kernel, const EpochArgs &A, const WaveGrap
     if constexpr (DIM <= 4) {
         if (A.same_table && G.col16) {
             hipLaunchKernelGGL((k_epoch_draw<DIM, NQ, true, true>), dim3((unsigned)grid), dim3(256), 0, s, A, G);
-            for (int32_t p = 0; p < G.n_phases; ++p)
+            for (int32_t p = 0; G.n_phases > 1 && p < G.n_phases; ++p)
                 hipLaunchKernelGGL((k_epoch_repulse<DIM>), dim3((unsigned)grid), dim3(256), 0, s, A, G, p);
             return hipGetLastError();
         }
@@ -494,7 +527,7 @@ static hipError_t launch_epoch_dq(int kernel, const EpochArgs &A, const WaveGrap
         hipLaunchKernelGGL((k_epoch_draw<DIM, NQ, true, false>), dim3((unsigned)grid), dim3(256), 0, s, A, G);
     else
         hipLaunchKernelGGL((k_epoch_draw<DIM, NQ, false, false>), dim3((unsigned)grid), dim3(256), 0, s, A, G);
-    for (int32_t p = 0; p < G.n_phases; ++p)
+    for (int32_t p = 0; G.n_phases > 1 && p < G.n_phases; ++p)
         hipLaunchKernelGGL((k_epoch_repulse<DIM>), dim3((unsigned)grid), dim3(256), 0, s, A, G, p);
     return hipGetLastError();
 }
