@@ -98,10 +98,12 @@ def test_transform_graph_init_and_epoch_parity():
         assert ei.value.code == U.UMAP_E_INVAL
 
 
-@pytest.mark.parametrize("n_table,dim", [(1_000_000, 2), (400_000, 3), (120_000, 16)])
-def test_transform_epoch_parity_large_table(n_table, dim):
-    """A table of several ranges (the negative samples are filed by range):
-    50,003 new points with 15 edges each to scattered table rows."""
+@pytest.mark.parametrize("n_table,dim,ranges", [(1_000_000, 2, 4), (700_000, 3, 4), (120_000, 16, 4),
+                                                (400_000, 3, 1)])
+def test_transform_epoch_parity_large_table(n_table, dim, ranges):
+    """Large tables: several ranges (the negative samples are filed by range)
+    or one range of 4.8 MB (each repulsion applied by the draw kernel): 50,003
+    new points with 15 edges each to scattered table rows."""
     n_new, k = 50_003, 15
     rng = np.random.default_rng(n_table + dim)
     start = rng.integers(0, n_table, size=(n_new, 1))
@@ -115,7 +117,7 @@ def test_transform_epoch_parity_large_table(n_table, dim):
     g = O.prep_bipartite(n_new, n_table, rows, cols, vals, N)
     with U.umap_transform_create(n_new, T, rows, cols, vals, a, b, N, R) as h:
         _check_graph(h, g)
-        assert U.umap_layout_stats(h)["table_ranges"] == 4
+        assert U.umap_layout_stats(h)["table_ranges"] == ranges
         # negatives are drawn from the table's rows
         got = U.umap_layout_debug_negatives(h, 9, 7, 1000, 5000)
         assert np.array_equal(got, O.negative_vertices(9, 7, 1000, 5000, R, n_table))
