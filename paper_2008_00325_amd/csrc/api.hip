@@ -402,7 +402,9 @@ int run_epochs_impl(umap_layout *h, uint64_t seed, int32_t first, int32_t last, 
     if (kernel == kAsyncKernel && (int64_t)h->max_degree + ul::kWaveCost >= ((int64_t)1 << 24))
         return fail(UMAP_E_INVAL, "the per-edge asynchronous kernel needs rows of fewer than %d edges",
                     (1 << 24) - ul::kWaveCost);
-    const bool records = kernel == 0;
+    // with one table range the draw kernel applies every negative itself and
+    // files no records, so no slot can overflow and no redo is needed
+    const bool records = kernel == 0 && h->lg_phases > 0;
     const int cur0 = h->cur;
     const size_t row_bytes = sizeof(float) * (size_t)h->dim;
     const size_t nd_bytes = row_bytes * (size_t)h->n;
