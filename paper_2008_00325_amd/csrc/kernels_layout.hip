@@ -445,26 +445,57 @@ __global__ __launch_bounds__(256) void k_epoch_repulse(EpochArgs A, WaveGraph G,
     long long *acc = s_acc[wv];
     float *yrows = s_y[wv];
     const size_t g0 = (size_t)r0 * DIM;
-    for (int t = lane; t < nrows * DIM; t += kWave) {
-        acc[lds_at<DIM, S>(t)] = A.in_place ? 0ll : G.delta[g0 + t];
-        yrows[lds_at<DIM, S>(t)] = A.E[g0 + t];
+    const uint32_t *recs = G.rec + roff + (int64_t)phase * cap;
+    const uint32_t base = range_base((uint32_t)phase, G.lg_phases, A.n_table);
+    // kRepUnroll records per lane per step, all loads issued before use.  The
+    // first step's record loads and gathers are issued around the loads of the
+    // wave's rows and sums, so that those latencies overlap.
+    constexpr int kRepUnroll = rep_unroll<DIM>();
+    uint32_t r[kRepUnroll];
+    float yk[kRepUnroll][DIM];
+    if (nrec > 0) {
+#pragma unroll
+        for (int u = 0; u < kRepUnroll; ++u) {
+            const int64_t t = u * kWave + lane;
+            r[u] = recs[t < nrec ? t : 0];
+        }
+    }
+    constexpr int kStage = (CAP * DIM + kWave - 1) / kWave;   // a wave holds at most CAP rows
+    long long dv[kStage];
+    float yv[kStage];
+#pragma unroll
+    for (int q = 0; q < kStage; ++q) {
+        const int t = q * kWave + (int)lane;
+        if (t < nrows * DIM) {
+            dv[q] = A.in_place ? 0ll : G.delta[g0 + t];
+            yv[q] = A.E[g0 + t];
+        }
+    }
+    if (nrec > 0) {
+#pragma unroll
+        for (int u = 0; u < kRepUnroll; ++u) load_row<DIM>(A.T, base + (r[u] & 0xFFFFFFu), yk[u]);
+    }
+#pragma unroll
+    for (int q = 0; q < kStage; ++q) {
+        const int t = q * kWave + (int)lane;
+        if (t < nrows * DIM) {
+            acc[lds_at<DIM, S>(t)] = dv[q];
+            yrows[lds_at<DIM, S>(t)] = yv[q];
+        }
     }
     wave_sync();
 
-    const uint32_t *recs = G.rec + roff + (int64_t)phase * cap;
-    const uint32_t base = range_base((uint32_t)phase, G.lg_phases, A.n_table);
-    // kRepUnroll records per lane per step, all loads issued before use
-    constexpr int kRepUnroll = rep_unroll<DIM>();
     for (int64_t b = 0; b < nrec; b += kRepUnroll * kWave) {
-        uint32_t r[kRepUnroll];
+        if (b > 0) {
 #pragma unroll
-        for (int u = 0; u < kRepUnroll; ++u) {
-            const int64_t t = b + u * kWave + lane;
-            r[u] = recs[t < nrec ? t : 0];
+            for (int u = 0; u < kRepUnroll; ++u) {
+                const int64_t t = b + u * kWave + lane;
+                r[u] = recs[t < nrec ? t : 0];
+            }
+#pragma unroll
+            for (int u = 0; u < kRepUnroll; ++u) load_row<DIM>(A.T, base + (r[u] & 0xFFFFFFu), yk[u]);
         }
-        float yi[kRepUnroll][DIM], yk[kRepUnroll][DIM];
-#pragma unroll
-        for (int u = 0; u < kRepUnroll; ++u) load_row<DIM>(A.T, base + (r[u] & 0xFFFFFFu), yk[u]);
+        float yi[kRepUnroll][DIM];
 #pragma unroll
         for (int u = 0; u < kRepUnroll; ++u) {
             const int h = (int)(r[u] >> 24);
