@@ -229,13 +229,23 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
     const int64_t lo = r0 >= halo ? r0 - halo : 0;
     const int64_t hi = r0 + nrows + halo <= (int64_t)A.n ? r0 + nrows + halo : (int64_t)A.n;
     for (int t = lane; t < nrows * S; t += kWave) acc[t] = 0;
-    if constexpr (S == DIM) {
-        for (int64_t t = (lo - r0) * DIM + lane; t < (hi - r0) * DIM; t += kWave) yrows[t] = A.E[(int64_t)g0 + t];
-    } else {
-        for (int t = lane; t < (int)(hi - lo) * DIM; t += kWave)
-            yrows[((int)(lo - r0) + t / DIM) * S + t % DIM] = A.E[(int64_t)lo * DIM + t];
-    }
     if ((int)lane < kMaxPhases) rec_n[lane] = 0;
+    {
+        // all of a lane's row loads are issued before the first LDS store
+        constexpr int kStageD = ((CAP + 2 * kHaloW) * DIM + kWave - 1) / kWave;
+        float yv[kStageD];
+        const int nst = (int)(hi - lo) * DIM;
+#pragma unroll
+        for (int q = 0; q < kStageD; ++q) {
+            const int t = q * kWave + (int)lane;
+            if (t < nst) yv[q] = A.E[(int64_t)lo * DIM + t];
+        }
+#pragma unroll
+        for (int q = 0; q < kStageD; ++q) {
+            const int t = q * kWave + (int)lane;
+            if (t < nst) yrows[((int)(lo - r0) + t / DIM) * S + t % DIM] = yv[q];
+        }
+    }
 
     // ---- classify and compact ----------------------------------------------
     // The wave's edges are addressed by 32-bit offsets from e0 (fewer than
