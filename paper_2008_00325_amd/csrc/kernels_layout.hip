@@ -193,8 +193,12 @@ __device__ __forceinline__ uint32_t range_base(uint32_t p, int32_t lg, uint32_t 
 // FIT: the tails and negatives index the moving layout itself (a fit: near
 // tails from LDS, self draws skipped, both shares of the attraction); else they
 // index a frozen table (a transform).  C16: the tails are read as 16-bit
-// offsets from their rows (G.col16), 2 bytes per edge instead of 4.
-template <int DIM, int NQ, bool FIT, bool C16>
+// offsets from their rows (G.col16), 2 bytes per edge instead of 4.  FUSED:
+// the table is one range (G.n_phases == 1) and each negative's repulsion is
+// applied here; a separate instance, so that the record-filing kernel of
+// several ranges carries none of its registers (at 8 components the draw
+// launch took 222 instead of 186 us with both paths in one kernel).
+template <int DIM, int NQ, bool FIT, bool C16, bool FUSED>
 __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
 {
     constexpr int CAP = rows_cap(DIM);
@@ -282,7 +286,7 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
     uint32_t *const rec_wave = G.rec + roff;   // this wave's slots, range p from p * cap
     // One table range: the whole table stays in L2 beside the edge stream, so
     // each negative's repulsion is applied here (no records, no range launch)
-    const bool fused = G.n_phases == 1;
+    constexpr bool fused = FUSED;
     uint2 *q = s_q[wv];
     uint32_t qhead = 0, qtail = 0;
     bool overflow = false;   // a record found its range's slots full
@@ -545,6 +549,15 @@ int32_t phase_log2(int64_t n, int32_t dim)
     return lg_bytes < lg_rows ? lg_bytes : lg_rows;
 }
 
+template <int DIM, int NQ, bool FIT, bool C16>
+static void launch_draw(int64_t grid, const EpochArgs &A, const WaveGraph &G, hipStream_t s)
+{
+    if (G.n_phases == 1)
+        hipLaunchKernelGGL((k_epoch_draw<DIM, NQ, FIT, C16, true>), dim3((unsigned)grid), dim3(256), 0, s, A, G);
+    else
+        hipLaunchKernelGGL((k_epoch_draw<DIM, NQ, FIT, C16, false>), dim3((unsigned)grid), dim3(256), 0, s, A, G);
+}
+
 template <int DIM, int NQ>
 static hipError_t launch_epoch_dq(int kernel, const EpochArgs &A, const WaveGraph &G, hipStream_t s)
 {
@@ -559,16 +572,16 @@ static hipError_t launch_epoch_dq(int kernel, const EpochArgs &A, const WaveGrap
     // the 16-bit tail stream is compiled for the common widths (1-4 components)
     if constexpr (DIM <= 4) {
         if (A.same_table && G.col16) {
-            hipLaunchKernelGGL((k_epoch_draw<DIM, NQ, true, true>), dim3((unsigned)grid), dim3(256), 0, s, A, G);
+            launch_draw<DIM, NQ, true, true>(grid, A, G, s);
             for (int32_t p = 0; G.n_phases > 1 && p < G.n_phases; ++p)
                 hipLaunchKernelGGL((k_epoch_repulse<DIM>), dim3((unsigned)grid), dim3(256), 0, s, A, G, p);
             return hipGetLastError();
         }
     }
     if (A.same_table)
-        hipLaunchKernelGGL((k_epoch_draw<DIM, NQ, true, false>), dim3((unsigned)grid), dim3(256), 0, s, A, G);
+        launch_draw<DIM, NQ, true, false>(grid, A, G, s);
     else
-        hipLaunchKernelGGL((k_epoch_draw<DIM, NQ, false, false>), dim3((unsigned)grid), dim3(256), 0, s, A, G);
+        launch_draw<DIM, NQ, false, false>(grid, A, G, s);
     for (int32_t p = 0; G.n_phases > 1 && p < G.n_phases; ++p)
         hipLaunchKernelGGL((k_epoch_repulse<DIM>), dim3((unsigned)grid), dim3(256), 0, s, A, G, p);
     return hipGetLastError();
