@@ -487,6 +487,43 @@ def test_every_width_both_kernels(dim):
     assert np.array_equal(outs[0].view(np.uint32), outs[1].view(np.uint32)), dim
 
 
+@pytest.fixture(scope="module")
+def window1m_prep(window1m_graph):
+    w, ids, dist, (r, c, v) = window1m_graph
+    return O.prep(w.n, r, c, v, w.n_epochs)
+
+
+@pytest.mark.parametrize("dim", list(range(2, 17)))
+def test_every_width_several_ranges(dim, window1m_graph, window1m_prep):
+    # every width from 2 on with a table of several ranges (the 1M window
+    # graph: 8 MB and more, 4 ranges), where the draw kernel files records and
+    # the range launches apply them: 20,000 sampled rows of one epoch against
+    # the oracle, and the two kernels bit for bit on the whole layout
+    w, ids, dist, (r, c, v) = window1m_graph
+    g = window1m_prep
+    N, R, ep, seed = w.n_epochs, w.neg_rate, 9, 23
+    print(f"[gpu case] width {dim}, 1M vertices, several table ranges", flush=True)
+    E = synth.embedding_state(w.n, dim, 500 + dim, 10.0)
+    rows = np.sort(np.random.default_rng(dim).choice(w.n, size=20_000, replace=False)).astype(np.int64)
+    ref = E[rows].astype(np.float64) + O.epoch_rows(g, E, ep, A_DEF, B_DEF, N, R, seed, rows)
+    outs = []
+    with U.umap_layout_create(w.n, dim, r, c, v, A_DEF, B_DEF, N, R) as h:
+        assert U.umap_layout_stats(h)["table_ranges"] == 4
+        for kernel in (0, 1):
+            U.umap_layout_set_kernel(h, kernel)
+            U.umap_layout_set_embedding(h, E)
+            U.umap_layout_run_epochs(h, seed, ep, ep + 1)
+            got = U.umap_layout_get(h)
+            st = U.umap_layout_stats(h)
+            assert st["overflow_redone"] == 0
+            assert st["active_edges"] == int(O.active_mask(g.eps, ep).sum())
+            err = float(np.abs(got[rows].astype(np.float64) - ref).max())
+            print(f"  kernel {kernel}: max|diff| = {err:.3e}", flush=True)
+            assert err <= TOL, (dim, kernel)
+            outs.append(got)
+    assert np.array_equal(outs[0].view(np.uint32), outs[1].view(np.uint32)), dim
+
+
 # ---------------------------------------------------------------------------
 # whole runs
 # ---------------------------------------------------------------------------
