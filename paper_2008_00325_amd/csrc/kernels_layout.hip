@@ -7,9 +7,10 @@
 // scatter to global memory, no atomics on the embedding in global memory).
 // In a transform the tails and negative samples are rows of a frozen layout T
 // (the trained embedding) and only the new points, the rows of E, move.
-//  * edge-parallel (default): one k_epoch_draw launch and P k_epoch_repulse
-//    launches per epoch, each wavefront owning a range of whole rows (see the
-//    section comment below).
+//  * edge-parallel (default): one k_epoch_draw launch and, when the vertex
+//    table is split into P > 1 ranges, P k_epoch_repulse launches per epoch,
+//    each wavefront owning a range of whole rows (see the section comment
+//    below).
 //  * k_epoch_rowwise: one thread per vertex walking its row (a plain second
 //    implementation used to cross-check the first).
 // Because the sums are exact integers, both paths give the same bits.
@@ -144,7 +145,9 @@ __global__ __launch_bounds__(256) void k_epoch_rowwise(EpochArgs A, const int64_
 //    of them or, at 1-2 components, within 64 rows of them),
 //    draws the edge's negative samples and files each one as a 4-byte record
 //    under the range of the vertex table it falls in.  The accumulator goes
-//    to delta.
+//    to delta.  With a table of one range (P = 1) the draw kernel's FUSED
+//    instance gathers each negative's row itself, adds its repulsion to the
+//    accumulator and commits E_{n+1}: no records and no range launch.
 //  * k_epoch_repulse (range p) reads the wave's records of range p and adds
 //    their repulsions.  All gathers of one launch hit one 1/P slice of the
 //    vertex table, which is sized to stay resident in an XCD's L2.  The last
