@@ -503,20 +503,33 @@ hipError_t launch_partition(const int64_t *row_ptr, int64_t r0, int64_t r1, int3
     return hipGetLastError();
 }
 
-// delta[e] = col[e] - (row of e) in 16 bits, one thread per row; *wide gets
-// 1 when some delta does not fit (then the wave kernels read the 32-bit
-// columns and delta is not used).
-__global__ void k_col_delta(const int64_t *__restrict__ row_ptr, const int32_t *__restrict__ col, int64_t n,
-                            int16_t *__restrict__ delta, unsigned *__restrict__ wide)
+// delta[e] = col[e] - (row of e) in 16 bits; *wide gets 1 when some delta
+// does not fit (then the wave kernels read the 32-bit columns and delta is not
+// used).  One block per 256 rows reads and writes the rows' edges with
+// consecutive threads on consecutive edges and finds each edge's row by a
+// binary search over the rows' starts staged in LDS (one thread walking a
+// whole row waits on one load per edge: 454 us at 1M vertices, k = 15).
+__global__ __launch_bounds__(256) void k_col_delta(const int64_t *__restrict__ row_ptr, const int32_t *__restrict__ col,
+                                                   int64_t n, int16_t *__restrict__ delta, unsigned *__restrict__ wide)
 {
-    const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    __shared__ int64_t s_rp[257];
+    const int64_t r0 = (int64_t)blockIdx.x * 256;
+    const int nr = (int)(n - r0 < 256 ? n - r0 : 256);
+    for (int t = threadIdx.x; t <= nr; t += 256) s_rp[t] = row_ptr[r0 + t];
+    __syncthreads();
+    const int64_t e1 = s_rp[nr];
     bool w = false;
-    if (r < n) {
-        for (int64_t e = row_ptr[r]; e < row_ptr[r + 1]; ++e) {
-            const int64_t d = (int64_t)col[e] - r;
-            w |= d < INT16_MIN || d > INT16_MAX;
-            delta[e] = (int16_t)d;
+    for (int64_t e = s_rp[0] + threadIdx.x; e < e1; e += 256) {
+        // the row of e: the last of the block's rows that starts at or before
+        // e (an empty row shares its start with the next row)
+        int lo = 0, hi = nr - 1;
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (s_rp[mid] <= e) lo = mid; else hi = mid - 1;
         }
+        const int64_t d = (int64_t)col[e] - (r0 + lo);
+        w |= d < INT16_MIN || d > INT16_MAX;
+        delta[e] = (int16_t)d;
     }
     if (__ballot(w) != 0 && (threadIdx.x & 63) == 0) atomicOr(wide, 1u);
 }
