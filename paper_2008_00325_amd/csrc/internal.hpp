@@ -139,17 +139,20 @@ constexpr int64_t kPhaseRows = 2500000;
 // With one range the draw kernel applies the repulsions itself (no records,
 // no partial sums, one launch per epoch), which beats the range launches for
 // tables up to kOneRangeBytes (200 epochs of window graphs, ms, one range
-// against the split: 2 components 400K vertices 18.2 / 29.5, 700K 37.6 /
-// 46.2, 800K 49.2 / 51.5, 900K 61.5 / 56.3; 3 components 400K 23.4 / 30.6;
-// 8 components 180K 28.0 / 29.3), and up to kOneRangeBytesWide from 9
-// components on (12 components 100K 22.4 / 22.7, 16 components 90K 27.4 /
-// 26.9).
+// against the split: 2 components 700K vertices 37.3 / 45.5; 3 components 500K
+// 32.6 / 38.1; 4 components 350K 26.3 / 31.3; 8 components 180K 27.8 / 28.1),
+// and up to kOneRangeBytesWide from 9 to kOneRangeMaxDim components (10
+// components 100K 21.2 / 21.5, 12 components 80K 18.5 / 19.0, 13 components
+// 75K 19.0 / 19.3).  Wider rows keep the plain rule (one range up to 2 MB):
+// 14 components 70K 19.7 / 19.4, 16 components 60K / 45K / 35K 20.0 / 18.9,
+// 15.6 / 15.1, 13.2 / 13.0.
 constexpr int64_t kOneRangeBytes = 6 << 20;
 constexpr int64_t kOneRangeBytesWide = 4 << 20;
+constexpr int32_t kOneRangeMaxDim = 13;
 // log2 of the number of ranges for a table of n vertices x dim: 0 up to
-// kOneRangeBytes (kOneRangeBytesWide above 8 components); else min(the ranges
-// that bring a range to kPhaseTableBytes, 4 ranges per kPhaseRows vertices
-// rounded up to a power of two, kMaxPhases).
+// kOneRangeBytes (kOneRangeBytesWide from 9 to kOneRangeMaxDim components);
+// else min(the ranges that bring a range down to kPhaseTableBytes, 4 ranges per
+// kPhaseRows vertices rounded up to a power of two), at most kMaxPhases.
 int32_t phase_log2(int64_t n, int32_t dim);
 
 hipError_t launch_epoch(int kernel, int32_t dim, const EpochArgs &A, const WaveGraph &G, hipStream_t s);

@@ -552,7 +552,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(rep_waves<D
 int32_t phase_log2(int64_t n, int32_t dim)
 {
     const int64_t bytes = n * dim * (int64_t)sizeof(float);
-    if (bytes <= (dim <= 8 ? kOneRangeBytes : kOneRangeBytesWide)) return 0;
+    if (bytes <= (dim <= 8 ? kOneRangeBytes : dim <= kOneRangeMaxDim ? kOneRangeBytesWide : 0)) return 0;
     int32_t lg_bytes = 0;   // the fewest ranges that bring a range down to kPhaseTableBytes
     while ((1 << (lg_bytes + 1)) <= kMaxPhases && (bytes >> lg_bytes) > kPhaseTableBytes) ++lg_bytes;
     int32_t lg_rows = 2;    // 4 ranges up to kPhaseRows vertices, twice as many per doubling of n beyond

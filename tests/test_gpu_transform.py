@@ -99,11 +99,12 @@ def test_transform_graph_init_and_epoch_parity():
 
 
 @pytest.mark.parametrize("n_table,dim,ranges", [(1_000_000, 2, 4), (700_000, 3, 4), (120_000, 16, 4),
-                                                (400_000, 3, 1)])
+                                                (400_000, 3, 1), (50_000, 16, 2)])
 def test_transform_epoch_parity_large_table(n_table, dim, ranges):
-    """Large tables: several ranges (the negative samples are filed by range)
-    or one range of 4.8 MB (each repulsion applied by the draw kernel): 50,003
-    new points with 15 edges each to scattered table rows."""
+    """Large tables: several ranges (the negative samples are filed by range),
+    one range of 4.8 MB (each repulsion applied by the draw kernel), or two
+    ranges of a 3.2 MB table at 16 components (one range only up to 2 MB at
+    that width): 50,003 new points with 15 edges each to scattered table rows."""
     n_new, k = 50_003, 15
     rng = np.random.default_rng(n_table + dim)
     start = rng.integers(0, n_table, size=(n_new, 1))
