@@ -69,8 +69,10 @@ typedef struct {
     double prep_ms;         /* device time of the ingest inside create           */
     double init_ms;         /* device time of the random initialisation (run)    */
     double epochs_ms;       /* device time of the last call's epoch launches     */
-    int32_t table_ranges;   /* P: an epoch is one draw launch and P repulsion
-                               launches, each gathering from 1/P of the table   */
+    int32_t table_ranges;   /* P: an epoch is one draw launch and, for P > 1,
+                               P repulsion launches, each gathering from 1/P of
+                               the table (with P = 1 the draw launch applies
+                               the negative samples itself)                     */
     int32_t kernel;         /* epoch kernel in use (see umap_layout_set_kernel)  */
     int32_t overflow_redone; /* 1 when the last call's epochs were redone by the
                                one-thread-per-vertex kernel because a negative
