@@ -437,10 +437,12 @@ __global__ __launch_bounds__(256) void k_epoch_draw(EpochArgs A, WaveGraph G)
 
 // Waves per SIMD the repulsion kernel's registers are held to: at 1-2
 // components 96 instead of 98 registers give a fifth wave per SIMD (window
-// graphs: 50.6 -> 50.3 us per launch at 1M vertices, 183.8 -> 180.6 us at 5M);
-// other widths keep the compiler's choice.
+// graphs: 50.6 -> 50.3 us per launch at 1M vertices, 183.8 -> 180.6 us at 5M),
+// at 16 components 76 instead of 109 (1M vertices: 191.0 -> 185.7 us); other
+// widths keep the compiler's choice (at 15 components the cap measured 230.3
+// against 228.1 us, at 8 components 125.0 against 124.2).
 template <int DIM>
-constexpr int rep_waves() { return DIM <= 2 ? 5 : 1; }
+constexpr int rep_waves() { return DIM <= 2 || DIM == 16 ? 5 : 1; }
 
 template <int DIM>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(rep_waves<DIM>(), 8))) void k_epoch_repulse(
